@@ -1,0 +1,24 @@
+"""CPU oracle for the HSA active-token layer step (test infrastructure only).
+
+Only the tests, the package smoke check and the benchmark's CPU-baseline leg
+import this package; the product path never does. It shares no code with the
+HIP library.
+"""
+
+from .hsa_oracle import (  # noqa: F401
+    active_set,
+    attention,
+    attention_output,
+    cached_euler,
+    check_budgets,
+    euler_delta,
+    layer_step,
+    mean_steps,
+    project,
+    qkv_cache_update,
+    round_bf16,
+    round_f32,
+    round_to,
+    trajectory,
+    window_margin,
+)

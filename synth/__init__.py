@@ -1,0 +1,19 @@
+"""Seeded synthetic workloads for the HSA active-token layer step.
+
+This package only draws inputs (random latents, weights, budgets, caches) and
+describes the workload shapes. It holds none of the method's arithmetic: no
+active-set rule, no projection, no attention, no Euler update. Both the CPU
+oracle and the GPU path consume what it produces.
+"""
+
+from .workloads import (  # noqa: F401
+    WORKLOADS,
+    Workload,
+    assign_budgets,
+    bf16_tensor,
+    draw_block,
+    draw_cache,
+    draw_euler_state,
+    linear_sigmas,
+    to_bf16_values,
+)

@@ -1,0 +1,192 @@
+"""Workload shapes and seeded input draws for the HSA active-token layer step.
+
+Token counts follow the video-DiT patchify rule of the paper's preliminaries
+(Section 2.1): a VAE latent of F x H_l x W_l patchified with [1, 2, 2] gives
+N = F * (H_l/2) * (W_l/2) tokens. The grids below are already in token units
+(F x H_l/2 x W_l/2), e.g. 21 x 30 x 52 = 32760 tokens for Wan-2 at 480p and
+21 x 45 x 80 = 75600 at 720p.
+
+Nothing here implements the method: the active-set rule, the projections,
+attention and the cached Euler update live in the oracle and in the HIP
+library, separately. This module only draws random inputs, in a fixed order
+from a seeded generator, and assigns per-token step budgets (an input of the
+method, Section 2.2, Eq. 3) by ranking a seeded per-token norm.
+
+bf16 inputs are represented on the host as float32 arrays whose values are
+exactly representable in bf16 (rounded to nearest-even by torch's own
+conversion); `bf16_tensor` turns them into torch bf16 tensors losslessly.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One synthetic single-block workload.
+
+    groups: ((budget s_k, token fraction), ...) of the step-budget partition
+    (Section 2.2, Eq. 3); every budget divides T (Eq. 5).
+    C: channels of the Euler state. None means the block output itself is the
+    velocity (the Euler state is the block input, C = d).
+    iters: iterations at which the workload is measured or checked.
+    """
+
+    name: str
+    grid: tuple
+    d: int
+    heads: int
+    dh: int
+    dtype: str
+    T: int
+    groups: tuple
+    iters: tuple = ()
+    C: int | None = None
+    notes: str = field(default="", compare=False)
+
+    @property
+    def N(self) -> int:
+        return int(np.prod(self.grid))
+
+    @property
+    def euler_channels(self) -> int:
+        return self.d if self.C is None else self.C
+
+
+WORKLOADS = {
+    # Tiny fp32 self-attention block; full 8-iteration trajectory.
+    "tiny_f32": Workload(
+        "tiny_f32", (4, 16, 16), 256, 4, 64, "f32", 8,
+        ((8, 1 / 3), (4, 1 / 3), (2, 1 / 3)), iters=tuple(range(8)),
+        notes="N=1024, d=256, 4x64 heads, fp32; budgets {8,4,2} by velocity-norm thirds",
+    ),
+    # Wan-2.1-1.3B-shaped block: d=1536, 12 heads x 128.
+    "wan1.3b": Workload(
+        "wan1.3b", (21, 30, 52), 1536, 12, 128, "bf16", 40,
+        ((40, 0.25), (20, 0.25), (10, 0.25), (5, 0.25)), iters=(2,),
+        notes="N=32760, d=1536, 12x128, bf16; iteration 2 has 50% of tokens active",
+    ),
+    # Wan-2.1-14B-shaped block: d=5120, 40 heads x 128.
+    "wan14b": Workload(
+        "wan14b", (21, 30, 52), 5120, 40, 128, "bf16", 40,
+        ((40, 0.25), (20, 0.25), (10, 0.25), (5, 0.25)), iters=(1, 2, 8),
+        notes="N=32760, d=5120, 40x128, bf16; iterations 1/2/8 have 25/50/100% active",
+    ),
+    # 720p-shaped long sequence with a 16-channel fp32 Euler state.
+    "wan14b_720p": Workload(
+        "wan14b_720p", (21, 45, 80), 5120, 40, 128, "bf16", 40,
+        ((40, 0.25), (10, 0.25), (5, 0.5)), iters=(1,), C=16,
+        notes="N=75600, d=5120, 40x128, bf16; iteration 1 has 25% active; Euler over N x 16 fp32",
+    ),
+}
+
+
+def to_bf16_values(a: np.ndarray) -> np.ndarray:
+    """Round a float32 array to bf16 (torch's nearest-even conversion) and return
+    the rounded values as float32."""
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def bf16_tensor(a: np.ndarray) -> torch.Tensor:
+    """torch bf16 tensor holding the values of a bf16-valued float32 array."""
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16)
+    back = t.to(torch.float32).numpy()
+    if not np.array_equal(back, a, equal_nan=True):
+        raise ValueError("array is not bf16-valued")
+    return t
+
+
+def _normal(rng: np.random.Generator, shape, scale: float = 1.0) -> np.ndarray:
+    z = rng.standard_normal(shape, dtype=np.float32)
+    if scale != 1.0:
+        z *= np.float32(scale)
+    return z
+
+
+def draw_block(wl: Workload, seed: int = 0, n_tokens: int | None = None) -> dict:
+    """Draw the block inputs in the fixed order x, Wq, Wk, Wv, Wo, v_group.
+
+    x ~ N(0, 1) of shape [N, d]; W ~ N(0, 1/d) of shape [d, d] in the
+    [d_out, d_in] orientation (y = x W^T); v_group ~ N(0, 1) of shape [N, C],
+    whose per-token norms rank tokens into budget groups.
+    All arrays are float32; for bf16 workloads they are bf16-valued.
+    """
+    N = wl.N if n_tokens is None else int(n_tokens)
+    d = wl.d
+    rng = np.random.default_rng(seed)
+    x = _normal(rng, (N, d))
+    ws = [_normal(rng, (d, d), 1.0 / math.sqrt(d)) for _ in range(4)]
+    v_group = _normal(rng, (N, wl.euler_channels))
+    if wl.dtype == "bf16":
+        x = to_bf16_values(x)
+        ws = [to_bf16_values(w) for w in ws]
+    wq, wk, wv, wo = ws
+    return {"x": x, "wq": wq, "wk": wk, "wv": wv, "wo": wo, "v_group": v_group}
+
+
+def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np.ndarray:
+    """Per-token step budgets (int32[N]) for a budget partition.
+
+    Group sizes: floor(N * fraction) for every budget except the largest, which
+    takes the remaining tokens.
+    layout "scattered": tokens ranked by the L2 norm of their v_group row
+    (stable ascending sort, ties to the lower index); the lowest-norm block
+    gets the smallest budget and the highest-norm block the largest.
+    layout "contiguous": consecutive index ranges in ascending budget order,
+    the largest budget last (the reordered sequence of Section 2.5).
+    """
+    N = v_group.shape[0]
+    order_groups = sorted(groups, key=lambda g: g[0])  # ascending budget
+    sizes = [int(math.floor(N * f)) for _, f in order_groups[:-1]]
+    sizes.append(N - sum(sizes))
+    if min(sizes) < 0:
+        raise ValueError("group fractions exceed 1")
+    if layout == "scattered":
+        norms = np.sqrt(np.sum(v_group.astype(np.float64) ** 2, axis=1))
+        rank = np.argsort(norms, kind="stable")
+    elif layout == "contiguous":
+        rank = np.arange(N)
+    else:
+        raise ValueError(f"unknown layout {layout!r}")
+    budget = np.empty(N, dtype=np.int32)
+    start = 0
+    for (s, _), n in zip(order_groups, sizes):
+        budget[rank[start:start + n]] = s
+        start += n
+    return budget
+
+
+def linear_sigmas(T: int) -> np.ndarray:
+    """Noise levels sigma_j = (T - j) / T for j = 0..T (1 down to 0), float32."""
+    return (np.arange(T, -1, -1, dtype=np.float64) / T).astype(np.float32)
+
+
+def draw_cache(N: int, d: int, seed: int, dtype: str = "bf16") -> tuple:
+    """Synthetic per-layer cache contents (K_hat, V_hat), each [N, d] ~ N(0, 1).
+
+    Stands in for the rows a dense step at an earlier iteration left in the
+    cache: with x ~ N(0,1) and W ~ N(0, 1/d), projected rows are ~ N(0, 1) too.
+    """
+    rng = np.random.default_rng([seed, 0xCACE])
+    k = _normal(rng, (N, d))
+    v = _normal(rng, (N, d))
+    if dtype == "bf16":
+        k, v = to_bf16_values(k), to_bf16_values(v)
+    return k, v
+
+
+def draw_euler_state(N: int, C: int, n_fresh: int, seed: int) -> dict:
+    """fp32 latent x [N, C], velocity cache [N, C] and fresh velocities
+    [n_fresh, C], all ~ N(0, 1)."""
+    rng = np.random.default_rng([seed, 0xE01E])
+    return {
+        "x": _normal(rng, (N, C)),
+        "v_cache": _normal(rng, (N, C)),
+        "v_fresh": _normal(rng, (n_fresh, C)),
+    }
