@@ -1,0 +1,95 @@
+// Internal helpers shared by the HIP translation units of the HSA step library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hsa {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // 16 raw bytes
+
+constexpr int kWave = 64;
+constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin over them
+
+// Map a linear workgroup id to a work item so that the items given to one XCD
+// are contiguous: workgroup L runs on XCD L % 8, and the i-th workgroup an XCD
+// receives gets item (first item of that XCD) + i. Bijective on [0, total).
+__device__ __forceinline__ int xcd_contiguous(int L, int total) {
+  const int xcd = L % kXcds;
+  const int slot = L / kXcds;
+  const int base = total / kXcds;
+  const int rem = total % kXcds;
+  return xcd * base + (xcd < rem ? xcd : rem) + slot;
+}
+
+// Round fp32 to bf16, nearest-even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ bf16x4 to_bf16x4(f32x4 v) { return __builtin_convertvector(v, bf16x4); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+}  // namespace hsa
+
+// Launchers (host side, one per translation unit). Each returns the HIP error
+// of the launch.
+namespace hsa {
+
+hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int margin,
+                             int32_t* idx, int32_t* n_active, hipStream_t s);
+
+// C[crow(m)][n] = sum_k A[arow(m)][k] * B_z[n][k] for up to three (B, C, c_rows)
+// outputs sharing A. a_rows / c_rows may be null (identity); rows whose index is
+// outside [0, a_limit) / [0, c_limit) are skipped.
+struct RowGemmOut {
+  const void* B;
+  void* C;
+  const int32_t* c_rows;
+  int c_limit;
+};
+struct RowGemm {
+  const void* A;
+  const int32_t* a_rows;
+  int a_limit;
+  int M, Nc, K;  // rows of the product, output columns, reduction length
+  long lda, ldb, ldc;
+  RowGemmOut out[3];
+  int n_out;
+};
+hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s);
+
+// Output z of a RowGemm, selected field by field so that a kernel never
+// indexes its by-value argument dynamically (which would copy it to scratch).
+__device__ __forceinline__ RowGemmOut row_gemm_out(const RowGemm& g, int z) {
+  RowGemmOut o;
+  o.B = z == 0 ? g.out[0].B : (z == 1 ? g.out[1].B : g.out[2].B);
+  o.C = z == 0 ? g.out[0].C : (z == 1 ? g.out[1].C : g.out[2].C);
+  o.c_rows = z == 0 ? g.out[0].c_rows : (z == 1 ? g.out[1].c_rows : g.out[2].c_rows);
+  o.c_limit = z == 0 ? g.out[0].c_limit : (z == 1 ? g.out[1].c_limit : g.out[2].c_limit);
+  return o;
+}
+hipError_t launch_row_gemm_f32(const RowGemm& g, hipStream_t s);
+
+hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, void* o, int n_q,
+                                 int n_kv, int heads, int head_dim, float scale, hipStream_t s);
+hipError_t launch_attention_f32(const void* q, const void* k, const void* v, void* o, int n_q,
+                                int n_kv, int heads, int head_dim, float scale, hipStream_t s);
+
+hipError_t launch_cached_euler(float* x, float* v_cache, const float* v_fresh,
+                               const int32_t* idx, int n_active, long n_tokens, int channels,
+                               float dsig, hipStream_t s);
+
+}  // namespace hsa

@@ -1,0 +1,181 @@
+"""Python binding of libhsa_step.so (include/hsa_step.h), via ctypes.
+
+Argument marshalling only: every function takes torch tensors (device memory
+from PyTorch-ROCm) and scalars, passes raw pointers and the current HIP stream
+to the C entry point of the same name, and raises HsaStepError on a non-zero
+status. No computation happens here; there is no fallback path. Importing this
+module fails if the HIP library has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhsa_step.so")
+
+F32 = 0
+BF16 = 1
+
+_STATUS = {
+    0: "HSA_STEP_OK",
+    1: "HSA_STEP_ERR_NULL",
+    2: "HSA_STEP_ERR_SHAPE",
+    3: "HSA_STEP_ERR_BUDGET",
+    4: "HSA_STEP_ERR_DTYPE",
+    5: "HSA_STEP_ERR_ALIAS",
+    6: "HSA_STEP_ERR_WORKSPACE",
+    7: "HSA_STEP_ERR_LAUNCH",
+}
+
+
+class HsaStepError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        self.name = _STATUS.get(status, str(status))
+        super().__init__(f"{fn}: {self.name} ({lib().hsa_step_status_string(status).decode()})")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library. Raises ImportError if it was never built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2605_06892_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P, I32, I64, F, S = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+        sig = {
+            "hsa_step_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "hsa_build_active_set": (ctypes.c_int, [P, I64, I32, I32, I32, P, P, P, P]),
+            "hsa_qkv_scatter": (ctypes.c_int, [ctypes.c_int, P, I32, P, I32, I64, I32, P, P, P, P, P, P, P]),
+            "hsa_attention_core": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P]),
+            "hsa_out_scatter": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P, P]),
+            "hsa_attention_workspace_bytes": (S, [ctypes.c_int, I32, I32]),
+            "hsa_active_attention": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P, S, P]),
+            "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+EXPORTED = (
+    "hsa_step_status_string",
+    "hsa_build_active_set",
+    "hsa_qkv_scatter",
+    "hsa_attention_core",
+    "hsa_out_scatter",
+    "hsa_attention_workspace_bytes",
+    "hsa_active_attention",
+    "hsa_cached_euler",
+)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype(*ts) -> int:
+    dts = {t.dtype for t in ts if t is not None}
+    if len(dts) != 1:
+        raise TypeError(f"tensors must share one dtype, got {dts}")
+    dt = dts.pop()
+    if dt == torch.bfloat16:
+        return BF16
+    if dt == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def _check(fn: str, st: int) -> None:
+    if st != 0:
+        raise HsaStepError(fn, st)
+
+
+def _dev(*ts) -> None:
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous device tensors")
+
+
+def hsa_build_active_set(budget, T: int, iteration: int, margin: int, idx, n_active_dev,
+                         read_back: bool = True, stream=None):
+    """Fill idx[:|A_i|] with the active set; returns |A_i| when read_back
+    (one stream synchronization), else None."""
+    _dev(budget, idx, n_active_dev)
+    host = ctypes.c_int32(-2)
+    st = lib().hsa_build_active_set(_ptr(budget), budget.numel(), T, iteration, margin, _ptr(idx),
+                                    _ptr(n_active_dev), ctypes.byref(host) if read_back else None,
+                                    _stream(stream))
+    _check("hsa_build_active_set", st)
+    return host.value if read_back else None
+
+
+def hsa_qkv_scatter(x, idx, n_active: int, wq, wk, wv, q_out, k_cache, v_cache,
+                    x_compact: bool = False, stream=None) -> None:
+    _dev(x, idx, wq, wk, wv, q_out, k_cache, v_cache)
+    dt = _dtype(x, wq, wk, wv, q_out, k_cache, v_cache)
+    n_tokens, d = k_cache.shape
+    st = lib().hsa_qkv_scatter(dt, _ptr(x), int(bool(x_compact)), _ptr(idx), n_active, n_tokens, d,
+                               _ptr(wq), _ptr(wk), _ptr(wv), _ptr(q_out), _ptr(k_cache), _ptr(v_cache),
+                               _stream(stream))
+    _check("hsa_qkv_scatter", st)
+
+
+def hsa_attention_core(q, k_cache, v_cache, n_active: int, heads: int, head_dim: int, scale: float,
+                       o, stream=None) -> None:
+    _dev(q, k_cache, v_cache, o)
+    dt = _dtype(q, k_cache, v_cache, o)
+    st = lib().hsa_attention_core(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_active, k_cache.shape[0],
+                                  heads, head_dim, scale, _ptr(o), _stream(stream))
+    _check("hsa_attention_core", st)
+
+
+def hsa_out_scatter(o, idx, n_active: int, wo, out, stream=None) -> None:
+    _dev(o, idx, wo, out)
+    dt = _dtype(o, wo, out)
+    n_tokens, d = out.shape
+    st = lib().hsa_out_scatter(dt, _ptr(o), _ptr(idx), n_active, n_tokens, d, _ptr(wo), _ptr(out),
+                               _stream(stream))
+    _check("hsa_out_scatter", st)
+
+
+def hsa_attention_workspace_bytes(dtype: torch.dtype, n_active: int, d: int) -> int:
+    return int(lib().hsa_attention_workspace_bytes(_dtype(torch.empty(0, dtype=dtype)), n_active, d))
+
+
+def hsa_active_attention(q, k_cache, v_cache, idx, n_active: int, heads: int, head_dim: int,
+                         scale: float, wo, out, workspace, stream=None) -> None:
+    _dev(q, k_cache, v_cache, idx, wo, out, workspace)
+    dt = _dtype(q, k_cache, v_cache, wo, out)
+    nbytes = workspace.numel() * workspace.element_size()
+    st = lib().hsa_active_attention(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(idx), n_active,
+                                    k_cache.shape[0], heads, head_dim, scale, _ptr(wo), _ptr(out),
+                                    _ptr(workspace), nbytes, _stream(stream))
+    _check("hsa_active_attention", st)
+
+
+def hsa_cached_euler(x, v_cache, v_fresh, idx, n_active: int, sigma_i: float, sigma_next: float,
+                     stream=None) -> None:
+    _dev(x, v_cache, v_fresh, idx)
+    for t in (x, v_cache, v_fresh):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("the cached Euler update is fp32")
+    n_tokens, channels = x.shape
+    st = lib().hsa_cached_euler(_ptr(x), _ptr(v_cache), _ptr(v_fresh), _ptr(idx), n_active, n_tokens,
+                                channels, sigma_i, sigma_next, _stream(stream))
+    _check("hsa_cached_euler", st)

@@ -1,0 +1,146 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+The library must load and export every entry point include/hsa_step.h
+declares, and every argument error must be reported with its documented
+status before anything is enqueued. Only error cases are called here (and the
+pure-host helpers), so no kernel is ever launched.
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hsa_step.h")
+
+H = pytest.importorskip("paper_2605_06892_amd.hsa_step")
+
+OK, NULL, SHAPE, BUDGET, DTYPE, ALIAS, WORKSPACE, LAUNCH = range(8)
+F32, BF16 = 0, 1
+# fake device addresses: never dereferenced, every call below fails validation first
+A = 0x7F0000000000
+B = 0x7F1000000000
+C = 0x7F2000000000
+D = 0x7F3000000000
+E = 0x7F4000000000
+G = 0x7F5000000000
+W = 0x7F6000000000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"^(?:int|size_t|const char\*)\s+(hsa_\w+)\s*\(", text, flags=re.M)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    try:
+        return H.lib()
+    except ImportError as e:  # pragma: no cover
+        pytest.fail(f"HIP library not built: {e}")
+
+
+def test_header_declares_the_four_hot_path_calls():
+    names = declared_functions()
+    for n in ("hsa_build_active_set", "hsa_qkv_scatter", "hsa_active_attention", "hsa_cached_euler"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(H.EXPORTED)
+    out = subprocess.run(["nm", "-D", "--defined-only", H._LIB_PATH], capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    assert set(names) <= exported
+    # nothing beyond the C ABI leaks out of the library
+    assert {s for s in exported if not s.startswith("_")} == set(names)
+
+
+def test_status_strings(lib):
+    for s in range(8):
+        assert lib.hsa_step_status_string(s)
+    assert lib.hsa_step_status_string(99) == b"unknown status"
+
+
+def test_workspace_bytes(lib):
+    assert lib.hsa_attention_workspace_bytes(BF16, 8190, 5120) == 8190 * 5120 * 2
+    assert lib.hsa_attention_workspace_bytes(F32, 10, 256) == 10 * 256 * 4
+    assert lib.hsa_attention_workspace_bytes(7, 10, 256) == 0
+    assert lib.hsa_attention_workspace_bytes(BF16, -1, 256) == 0
+
+
+def test_build_active_set_errors(lib):
+    f = lib.hsa_build_active_set
+    assert f(A, 100, 0, 0, 0, B, C, None, None) == BUDGET        # T < 1
+    assert f(A, 100, 40, 40, 0, B, C, None, None) == BUDGET      # iter >= T
+    assert f(A, 100, 40, -1, 0, B, C, None, None) == BUDGET
+    assert f(A, 100, 40, 0, 21, B, C, None, None) == BUDGET      # margin > T/2
+    assert f(A, 100, 40, 0, -1, B, C, None, None) == BUDGET
+    assert f(A, -1, 40, 0, 0, B, C, None, None) == SHAPE
+    assert f(A, 1 << 31, 40, 0, 0, B, C, None, None) == SHAPE
+    assert f(None, 100, 40, 0, 0, B, C, None, None) == NULL
+    assert f(A, 100, 40, 0, 0, None, C, None, None) == NULL
+    assert f(A, 100, 40, 0, 0, B, None, None, None) == NULL
+    assert f(A, 100, 40, 0, 0, A + 8, C, None, None) == ALIAS    # idx overlaps budget
+    assert f(A, 100, 40, 0, 0, B, B + 396, None, None) == ALIAS  # count inside idx
+
+
+def test_qkv_scatter_errors(lib):
+    f = lib.hsa_qkv_scatter
+    args = lambda **k: dict(dict(dt=BF16, x=A, xc=0, idx=B, n=10, N=100, d=256, wq=C, wk=D, wv=E,  # noqa: E731
+                                 q=G, kc=W, vc=W + 100 * 256 * 2), **k)
+    call = lambda a: f(a["dt"], a["x"], a["xc"], a["idx"], a["n"], a["N"], a["d"], a["wq"], a["wk"],  # noqa: E731
+                       a["wv"], a["q"], a["kc"], a["vc"], None)
+    assert call(args(dt=5)) == DTYPE
+    assert call(args(d=0)) == SHAPE
+    assert call(args(d=200)) == SHAPE       # bf16 needs d % 64 == 0
+    assert call(args(n=101)) == SHAPE       # more active rows than tokens
+    assert call(args(n=-1)) == SHAPE
+    assert call(args(x=None)) == NULL
+    assert call(args(wv=None)) == NULL
+    assert call(args(x=A + 2)) == SHAPE     # bf16 rows must be 16-byte aligned
+    assert call(args(q=A)) == ALIAS         # q_out on top of x
+    assert call(args(vc=W + 16)) == ALIAS   # the two caches overlap
+    assert call(args(kc=C)) == ALIAS        # cache on top of a weight
+
+
+def test_attention_errors(lib):
+    f = lib.hsa_attention_core
+    assert f(9, A, B, C, 10, 100, 4, 64, 0.125, D, None) == DTYPE
+    assert f(BF16, A, B, C, 10, 100, 4, 96, 0.125, D, None) == SHAPE   # head_dim not 64/128
+    assert f(BF16, A, B, C, 10, 100, 0, 64, 0.125, D, None) == SHAPE
+    assert f(BF16, A, B, C, 10, 0, 4, 64, 0.125, D, None) == SHAPE     # no keys
+    assert f(BF16, A, B, C, 10, 100, 4, 64, 0.0, D, None) == SHAPE     # scale must be > 0
+    assert f(BF16, A, B, C, 10, 100, 4, 64, float("nan"), D, None) == SHAPE
+    assert f(BF16, A, None, C, 10, 100, 4, 64, 0.125, D, None) == NULL
+    assert f(BF16, A, B, C, 10, 100, 4, 64, 0.125, A, None) == ALIAS   # o on top of q
+    assert f(BF16, A, B, C, 10, 100, 4, 64, 0.125, B + 512, None) == ALIAS
+    g = lib.hsa_active_attention
+    need = lib.hsa_attention_workspace_bytes(BF16, 10, 256)
+    assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, None, need, None) == WORKSPACE
+    assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, W, need - 1, None) == WORKSPACE
+    assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, G, need, None) == ALIAS
+    assert g(BF16, A, B, C, None, 10, 100, 4, 64, 0.125, E, G, W, need, None) == NULL
+    assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, None, W, need, None) == NULL
+    h = lib.hsa_out_scatter
+    assert h(BF16, A, B, 10, 100, 256, C, A, None) == ALIAS           # out on top of o
+    assert h(BF16, A, B, 10, 100, 100, C, D, None) == SHAPE
+    assert h(BF16, A, None, 10, 100, 256, C, D, None) == NULL
+
+
+def test_euler_errors(lib):
+    f = lib.hsa_cached_euler
+    assert f(A, B, None, None, 0, -1, 16, 1.0, 0.9, None) == SHAPE
+    assert f(None, B, None, None, 0, 100, 16, 1.0, 0.9, None) == NULL
+    assert f(A, B, C, None, 10, 100, 16, 1.0, 0.9, None) == NULL       # fresh rows need idx
+    assert f(A, B, C, D, 101, 100, 16, 1.0, 0.9, None) == SHAPE
+    assert f(A, A + 64, None, None, 0, 100, 16, 1.0, 0.9, None) == ALIAS
+    assert f(A, B, B + 4, D, 10, 100, 16, 1.0, 0.9, None) == ALIAS     # fresh inside the cache
+    # nothing to do is success without touching memory
+    assert f(None, None, None, None, 0, 0, 16, 1.0, 0.9, None) == OK
