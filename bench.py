@@ -1,0 +1,296 @@
+"""Benchmark of the HSA active-token layer step on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+  active set (with its one host read-back) -> Q/K/V + cache overwrite ->
+  active-query attention -> output projection + scatter -> cached Euler update
+of the N x 16 fp32 latents.
+
+Default workload: a Wan-2.1-14B-shaped block, N = 21 x 30 x 52 = 32760 tokens,
+d = 5120 (40 heads x 128), bf16, T = 40 with budgets {40, 20, 10, 5} on
+quarters of the tokens ranked by a seeded velocity norm; timed at iteration 1
+(25% of the tokens active) and, as a second line item, iteration 2 (50%).
+The KV cache is filled by a dense iteration 0 first (every token is active at
+i = 0). Inputs are synthetic (seeded normal latents and N(0, 1/d) weights);
+everything is resident in HBM before the timed region.
+
+Prints ONE JSON line. `value` is the layer-step time in ms (Q/K/V + cache
+overwrite + attention + output projection and scatter, GPU event time) at
+25% active; per-kernel times, the attention TFLOP/s at 25% and 50% active,
+the roofline of the attention kernel and the CPU oracle baseline are extra
+fields.
+
+    python bench.py [--steps K] [--warmup W] [--workload wan14b] [--no-cpu-baseline]
+    python bench.py --only attention --steps 3     # one kernel, for rocprofv3 counter passes
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "HSA layer-step ms + active-attention TFLOP/s at N=32760, 25%/50% active"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+EULER_CHANNELS = 16         # latent channels advanced by the cached Euler update
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_wan14b_traffic.txt")
+ATTN_SRC = os.path.join(ROOT, "paper_2605_06892_amd", "csrc", "attention_bf16.hip")
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="wan14b", choices=["wan14b", "wan1.3b", "wan14b_720p"])
+    p.add_argument("--iteration", type=int, default=1, help="timed iteration (1: 25%% active)")
+    p.add_argument("--second-iteration", type=int, default=2, help="also time this iteration (-1: skip)")
+    p.add_argument("--layout", default="scattered", choices=["scattered", "contiguous"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--only", default=None,
+                   choices=["active_set", "qkv", "attention", "out", "euler", "copy"],
+                   help="launch only this kernel --steps times after setup (profiling passes)")
+    return p.parse_args()
+
+
+def setup(wl, layout, dev):
+    import torch
+
+    import synth
+    from paper_2605_06892_amd import layer as L
+
+    blk = synth.draw_block(wl, 0)
+    budget = synth.assign_budgets(blk["v_group"], wl.groups, layout)
+    b = L.BlockBuffers.allocate(wl.N, wl.d, wl.heads, wl.dh, torch.bfloat16, device=dev)
+    b.x.copy_(synth.bf16_tensor(blk["x"]))
+    for k in ("wq", "wk", "wv", "wo"):
+        getattr(b, k).copy_(synth.bf16_tensor(blk[k]))
+    b.budget.copy_(torch.from_numpy(budget))
+    b.out.zero_()
+    st = synth.draw_euler_state(wl.N, EULER_CHANNELS, wl.N, seed=5)
+    eul = {k: torch.from_numpy(v).to(dev) for k, v in st.items()}
+    # dense iteration 0 fills the caches and the output rows
+    n0 = L.active_set(b, wl.T, 0)
+    assert n0 == wl.N
+    L.layer_step(b, n0)
+    torch.cuda.synchronize()
+    return blk, budget, b, eul
+
+
+def run_step(b, eul, T, it, sigmas, ev=None):
+    """One full pass of the hot path; if ev is given, record events between calls."""
+    from paper_2605_06892_amd import hsa_step as H
+    from paper_2605_06892_amd import layer as L
+
+    rec = (lambda k: ev[k].record()) if ev is not None else (lambda k: None)  # noqa: E731
+    rec(0)
+    n = L.active_set(b, T, it)
+    rec(1)
+    L.qkv(b, n)
+    rec(2)
+    L.attention(b, n)
+    rec(3)
+    L.out_projection(b, n)
+    rec(4)
+    H.hsa_cached_euler(eul["x"], eul["v_cache"], eul["v_fresh"], b.idx, n, float(sigmas[it]), float(sigmas[it + 1]))
+    rec(5)
+    return n
+
+
+def time_iteration(b, eul, wl, it, sigmas, steps, warmup):
+    import torch
+
+    for _ in range(warmup):
+        run_step(b, eul, wl.T, it, sigmas)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    n = 0
+    for s in range(steps):
+        n = run_step(b, eul, wl.T, it, sigmas, evs[s])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+    names = ["active_set", "qkv_scatter", "attention", "out_scatter", "cached_euler"]
+    per = {nm: float(np.mean([evs[s][k].elapsed_time(evs[s][k + 1]) for s in range(steps)]))
+           for k, nm in enumerate(names)}
+    return n, wall, per
+
+
+def attention_flops(n_active, N, d):
+    return 4.0 * n_active * N * d  # QK^T and PV, 2 FLOP per multiply-add
+
+
+def gemm_flops(n_active, d):
+    return 2.0 * n_active * d * (3 * d) + 2.0 * n_active * d * d
+
+
+def traffic_from_profile():
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    src_sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256") != src_sha:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, blk, budget, it):
+    """The oracle's layer step timed on this host: two bounded samples of the
+    active rows (projections, attention against the whole N-row cache, output
+    projection and scatter), extrapolated linearly to all active rows."""
+    import oracle
+    import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"), default=1)
+    except Exception:  # pragma: no cover
+        threads = 1
+    idx = oracle.active_set(budget, wl.T, it)
+    k0, v0 = synth.draw_cache(wl.N, wl.d, seed=1, dtype="bf16")
+    out0 = np.zeros((wl.N, wl.d), np.float32)
+    w = {k: blk[k] for k in ("wq", "wk", "wv", "wo")}
+    rng = np.random.default_rng(0)
+    times = {}
+    for s in (256, 512):
+        sub = np.sort(rng.choice(idx, size=min(s, idx.size), replace=False))
+        t0 = time.perf_counter()
+        oracle.layer_step(blk["x"], sub, w, k0, v0, out0, wl.heads, wl.dh, 1 / math.sqrt(wl.dh), "bf16")
+        times[s] = time.perf_counter() - t0
+    per_row = max((times[512] - times[256]) / 256.0, 0.0)
+    fixed = max(times[256] - 256 * per_row, 0.0)
+    est_ms = (fixed + per_row * idx.size) * 1e3
+    return {"value": round(est_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+            "host_cpus": os.cpu_count(),
+            "sample": (f"oracle.layer_step on 256 and 512 of the {idx.size} active rows (all {wl.N} cached rows, "
+                       f"{wl.heads} heads), {times[256]:.1f}s + {times[512]:.1f}s; linear fit extrapolated to "
+                       f"all {idx.size} active rows")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the layer step has no "
+              "multi-GPU path in this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import synth
+    from paper_2605_06892_amd import hsa_step as H
+    from paper_2605_06892_amd import layer as L
+
+    H.lib()  # fail loudly if the HIP library is missing
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    sigmas = synth.linear_sigmas(wl.T)
+    blk, budget, b, eul = setup(wl, args.layout, dev)
+
+    if args.only:
+        n = L.active_set(b, wl.T, args.iteration)
+        big = None
+        if args.only == "copy":
+            big = torch.empty(256 << 20, dtype=torch.float32, device=dev)  # 1 GiB
+            dst = torch.empty_like(big)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            if args.only == "active_set":
+                L.active_set(b, wl.T, args.iteration)
+            elif args.only == "qkv":
+                L.qkv(b, n)
+            elif args.only == "attention":
+                L.attention(b, n)
+            elif args.only == "out":
+                L.out_projection(b, n)
+            elif args.only == "euler":
+                H.hsa_cached_euler(eul["x"], eul["v_cache"], eul["v_fresh"], b.idx, n, float(sigmas[1]), float(sigmas[2]))
+            elif args.only == "copy":
+                dst.copy_(big)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": args.only, "steps": args.steps, "n_active": n,
+                          "copy_bytes": None if big is None else big.numel() * 4}))
+        return
+
+    n, wall, per = time_iteration(b, eul, wl, args.iteration, sigmas, args.steps, args.warmup)
+    layer_ms = per["qkv_scatter"] + per["attention"] + per["out_scatter"]
+    attn_fl = attention_flops(n, wl.N, wl.d)
+    attn_tflops = attn_fl / (per["attention"] * 1e-3) / 1e12
+    gemm_tf = gemm_flops(n, wl.d) / ((per["qkv_scatter"] + per["out_scatter"]) * 1e-3) / 1e12
+    euler_bytes = (wl.N * EULER_CHANNELS * 4 * 3) + n * EULER_CHANNELS * 4 * 2 + n * 4
+    out = {
+        "metric": METRIC,
+        "value": round(layer_ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name} single block: N={wl.N} ({'x'.join(map(str, wl.grid))} latent tokens), "
+                        f"d={wl.d} ({wl.heads}x{wl.dh} heads), T={wl.T}, budgets "
+                        f"{{{','.join(str(g[0]) for g in wl.groups)}}} by velocity-norm rank ({args.layout}), "
+                        f"iteration {args.iteration}",
+            "n_active": n,
+            "active_fraction": round(n / wl.N, 4),
+            "euler_state": f"{wl.N}x{EULER_CHANNELS} fp32",
+        },
+        "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "active_attention_tflops": round(attn_tflops, 2),
+        "qkv_out_gemm_tflops": round(gemm_tf, 2),
+        "euler_gbs": round(euler_bytes / (per["cached_euler"] * 1e-3) / 1e9, 1),
+    }
+    out["roofline"] = {
+        "kernel": "attention_bf16",
+        "bound": "mfma",
+        "achieved": round(attn_tflops, 2),
+        "peak": PEAK_BF16_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+        "traffic": traffic_from_profile(),
+        "flops_per_launch": attn_fl,
+    }
+    if args.second_iteration >= 0:
+        n2, wall2, per2 = time_iteration(b, eul, wl, args.second_iteration, sigmas, args.steps, 1)
+        out["second"] = {
+            "iteration": args.second_iteration,
+            "n_active": n2,
+            "active_fraction": round(n2 / wl.N, 4),
+            "layer_step_ms": round(per2["qkv_scatter"] + per2["attention"] + per2["out_scatter"], 4),
+            "ms_per_step": round(wall2, 4),
+            "kernels_ms": {k: round(v, 4) for k, v in per2.items()},
+            "active_attention_tflops": round(attention_flops(n2, wl.N, wl.d) / (per2["attention"] * 1e-3) / 1e12, 2),
+        }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, blk, budget, args.iteration)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()
