@@ -57,6 +57,10 @@ def parse():
     p.add_argument("--second-iteration", type=int, default=2, help="also time this iteration (-1: skip)")
     p.add_argument("--layout", default="scattered", choices=["scattered", "contiguous"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--summarize", metavar="DIR", default=None,
+                   help="print a text summary of the rocprofv3 csv output under DIR and exit")
+    p.add_argument("--write-traffic", metavar="DIR", default=None,
+                   help="from counter passes DIR/{attn,copy}_{fetch,write} write the attention HBM traffic file")
     p.add_argument("--only", default=None,
                    choices=["active_set", "qkv", "attention", "out", "euler", "copy"],
                    help="launch only this kernel --steps times after setup (profiling passes)")
@@ -79,10 +83,10 @@ def setup(wl, layout, dev):
     b.out.zero_()
     st = synth.draw_euler_state(wl.N, EULER_CHANNELS, wl.N, seed=5)
     eul = {k: torch.from_numpy(v).to(dev) for k, v in st.items()}
-    # dense iteration 0 fills the caches and the output rows
+    # iteration 0 activates every token: its Q/K/V pass fills the whole cache
     n0 = L.active_set(b, wl.T, 0)
     assert n0 == wl.N
-    L.layer_step(b, n0)
+    L.qkv(b, n0)
     torch.cuda.synchronize()
     return blk, budget, b, eul
 
@@ -153,6 +157,93 @@ def traffic_from_profile():
         return None
 
 
+def _csv_rows(path):
+    import csv
+
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _find(d, suffix):
+    out = []
+    for root, _, files in os.walk(d):
+        out += [os.path.join(root, f) for f in files if f.endswith(suffix)]
+    return sorted(out)
+
+
+def _short(name, n=90):
+    return name if len(name) <= n else name[: n - 3] + "..."
+
+
+def counter_means(d):
+    """{(kernel, counter): mean value per dispatch} from rocprofv3 counter csv files."""
+    acc = {}
+    for f in _find(d, "counter_collection.csv"):
+        for r in _csv_rows(f):
+            key = (r["Kernel_Name"], r["Counter_Name"])
+            acc.setdefault(key, []).append(float(r["Counter_Value"]))
+    return {k: (float(np.mean(v)), len(v)) for k, v in acc.items()}
+
+
+def summarize(d):
+    lines = []
+    for f in _find(d, "kernel_stats.csv"):
+        lines.append(f"kernel statistics ({os.path.relpath(f, d)})")
+        lines.append(f"{'calls':>6} {'avg_us':>10} {'min_us':>10} {'max_us':>10} {'pct':>6}  kernel")
+        for r in _csv_rows(f):
+            lines.append(f"{int(r['Calls']):>6} {float(r['AverageNs'])/1e3:>10.1f} {float(r['MinNs'])/1e3:>10.1f} "
+                         f"{float(r['MaxNs'])/1e3:>10.1f} {float(r['Percentage']):>6.2f}  {_short(r['Name'])}")
+    cm = counter_means(d)
+    if cm:
+        lines.append("counters (mean per dispatch)")
+        for (k, c), (v, n) in sorted(cm.items()):
+            lines.append(f"{c:>28} {v:>18.1f}  dispatches={n}  {_short(k)}")
+    return "\n".join(lines)
+
+
+def write_traffic(d):
+    """HBM bytes per attention launch: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) of the attention kernel, each scaled by expected/measured bytes
+    of a plain 1 GiB device copy profiled the same way."""
+    def mean_of(sub, counter, kernel_pred):
+        vals = [v for (k, c), (v, _) in counter_means(os.path.join(d, sub)).items()
+                if c == counter and kernel_pred(k)]
+        if not vals:
+            raise SystemExit(f"no {counter} data in {sub}")
+        return vals[0]
+    is_attn = lambda k: "attention_bf16_kernel" in k  # noqa: E731
+    is_copy = lambda k: "copy" in k.lower() or "elementwise" in k  # noqa: E731
+    copy_bytes = float(256 << 20) * 4
+    f_att = mean_of("attn_fetch", "FETCH_SIZE", is_attn) * 1024
+    w_att = mean_of("attn_write", "WRITE_SIZE", is_attn) * 1024
+    f_cpy = mean_of("copy_fetch", "FETCH_SIZE", is_copy) * 1024
+    w_cpy = mean_of("copy_write", "WRITE_SIZE", is_copy) * 1024
+    fetch_scale, write_scale = copy_bytes / f_cpy, copy_bytes / w_cpy
+    total = f_att * fetch_scale + w_att * write_scale
+    sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
+    text = (
+        "# HBM traffic of one attention launch (Wan-14B-shaped block, N=32760, d=5120, 25% active)\n"
+        "# from rocprofv3 counter passes, each command run from the repository root:\n"
+        "#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/attn_fetch -o run -- python3 bench.py --only attention --steps 3\n"
+        "#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/attn_write -o run -- python3 bench.py --only attention --steps 3\n"
+        "#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/copy_fetch -o run -- python3 bench.py --only copy --steps 3\n"
+        "#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/copy_write -o run -- python3 bench.py --only copy --steps 3\n"
+        "#   python3 bench.py --write-traffic <out>\n"
+        "# the copy passes move 1 GiB each way; their counters calibrate bytes per KiB unit\n"
+        f"attention_fetch_kib_per_dispatch: {f_att / 1024:.1f}\n"
+        f"attention_write_kib_per_dispatch: {w_att / 1024:.1f}\n"
+        f"copy_fetch_kib_per_dispatch: {f_cpy / 1024:.1f}\n"
+        f"copy_write_kib_per_dispatch: {w_cpy / 1024:.1f}\n"
+        f"fetch_scale: {fetch_scale:.4f}\n"
+        f"write_scale: {write_scale:.4f}\n"
+        f"hbm_bytes_per_launch: {total:.0f}\n"
+        f"kernel_source_sha256: {sha}\n"
+    )
+    with open(TRAFFIC_FILE, "w") as f:
+        f.write(text)
+    return text
+
+
 def cpu_baseline(wl, blk, budget, it):
     """The oracle's layer step timed on this host: two bounded samples of the
     active rows (projections, attention against the whole N-row cache, output
@@ -188,6 +279,12 @@ def cpu_baseline(wl, blk, budget, it):
 
 def main():
     args = parse()
+    if args.summarize:
+        print(summarize(args.summarize))
+        return
+    if args.write_traffic:
+        print(write_traffic(args.write_traffic))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the layer step has no "
               "multi-GPU path in this build", file=sys.stderr)

@@ -26,13 +26,17 @@ constexpr int BM = 128, BN = 128, BK = 64, kThreads = 256;
 constexpr int LS = BK + 8;  // LDS row stride in bf16 (144 bytes, 16-byte aligned)
 constexpr int kGroupM = 8;
 
+// NOUT (1 or 3) is the number of outputs sharing A; it is a template
+// parameter so the Q/K/V projection and the output projection are distinct
+// kernels in profiles.
+template <int NOUT>
 __global__ __launch_bounds__(kThreads, 2) void row_gemm_bf16_kernel(RowGemm g) {
   __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LS];
   __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LS];
 
   const int tiles_m = (g.M + BM - 1) / BM;
   const int tiles_n1 = (g.Nc + BN - 1) / BN;  // per output
-  const int tiles_n = tiles_n1 * g.n_out;     // over all outputs side by side
+  const int tiles_n = tiles_n1 * NOUT;        // over all outputs side by side
   const int total = tiles_m * tiles_n;
   const int item = xcd_contiguous(blockIdx.x, total);
   // grouped order: kGroupM tile-rows sweep all tile-columns together
@@ -151,9 +155,12 @@ __global__ __launch_bounds__(kThreads, 2) void row_gemm_bf16_kernel(RowGemm g) {
 }  // namespace
 
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
-  if (g.M <= 0 || g.Nc <= 0 || g.n_out <= 0) return hipSuccess;
+  if (g.M <= 0 || g.Nc <= 0 || (g.n_out != 1 && g.n_out != 3)) return hipSuccess;
   const long tiles = (long)((g.M + BM - 1) / BM) * ((g.Nc + BN - 1) / BN) * g.n_out;
-  hipLaunchKernelGGL(row_gemm_bf16_kernel, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
+  if (g.n_out == 3)
+    hipLaunchKernelGGL(row_gemm_bf16_kernel<3>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
+  else
+    hipLaunchKernelGGL(row_gemm_bf16_kernel<1>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
   return hipGetLastError();
 }
 
