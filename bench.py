@@ -175,14 +175,19 @@ def _short(name, n=90):
     return name if len(name) <= n else name[: n - 3] + "..."
 
 
-def counter_means(d):
-    """{(kernel, counter): mean value per dispatch} from rocprofv3 counter csv files."""
+def counter_values(d):
+    """{(kernel, counter): [value per dispatch]} from rocprofv3 counter csv files."""
     acc = {}
     for f in _find(d, "counter_collection.csv"):
         for r in _csv_rows(f):
             key = (r["Kernel_Name"], r["Counter_Name"])
             acc.setdefault(key, []).append(float(r["Counter_Value"]))
-    return {k: (float(np.mean(v)), len(v)) for k, v in acc.items()}
+    return acc
+
+
+def counter_means(d):
+    """{(kernel, counter): (mean value per dispatch, dispatches)}."""
+    return {k: (float(np.mean(v)), len(v)) for k, v in counter_values(d).items()}
 
 
 def summarize(d):
@@ -205,19 +210,20 @@ def write_traffic(d):
     """HBM bytes per attention launch: FETCH_SIZE and WRITE_SIZE (KiB per
     dispatch) of the attention kernel, each scaled by expected/measured bytes
     of a plain 1 GiB device copy profiled the same way."""
-    def mean_of(sub, counter, kernel_pred):
-        vals = [v for (k, c), (v, _) in counter_means(os.path.join(d, sub)).items()
-                if c == counter and kernel_pred(k)]
+    def values(sub, counter, kernel_pred):
+        vals = [v for (k, c), vs in counter_values(os.path.join(d, sub)).items()
+                if c == counter and kernel_pred(k) for v in vs]
         if not vals:
             raise SystemExit(f"no {counter} data in {sub}")
-        return vals[0]
+        return vals
     is_attn = lambda k: "attention_bf16_kernel" in k  # noqa: E731
-    is_copy = lambda k: "copy" in k.lower() or "elementwise" in k  # noqa: E731
+    is_copy = lambda k: "copyBuffer" in k  # noqa: E731
     copy_bytes = float(256 << 20) * 4
-    f_att = mean_of("attn_fetch", "FETCH_SIZE", is_attn) * 1024
-    w_att = mean_of("attn_write", "WRITE_SIZE", is_attn) * 1024
-    f_cpy = mean_of("copy_fetch", "FETCH_SIZE", is_copy) * 1024
-    w_cpy = mean_of("copy_write", "WRITE_SIZE", is_copy) * 1024
+    f_att = float(np.mean(values("attn_fetch", "FETCH_SIZE", is_attn))) * 1024
+    w_att = float(np.mean(values("attn_write", "WRITE_SIZE", is_attn))) * 1024
+    # the 1 GiB copies are the largest copy dispatches of their runs
+    f_cpy = max(values("copy_fetch", "FETCH_SIZE", is_copy)) * 1024
+    w_cpy = max(values("copy_write", "WRITE_SIZE", is_copy)) * 1024
     fetch_scale, write_scale = copy_bytes / f_cpy, copy_bytes / w_cpy
     total = f_att * fetch_scale + w_att * write_scale
     sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
