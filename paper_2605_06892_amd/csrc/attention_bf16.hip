@@ -2,79 +2,110 @@
 // for every active row j and head h, o[j,h] = softmax(scale q[j,h] K_h^T) V_h
 // over all N cached rows. Cost O(|A_i| N d) instead of O(N^2 d).
 //
-// Work split: one workgroup of NW waves per (head, tile of NW*32*QT active
-// queries); each wave owns 32*QT queries. Workgroups of one head are placed
+// Work split: one workgroup of NW waves per (head, tile of 32*NW active
+// queries); each wave owns 32 queries. Workgroups of one head are placed
 // contiguously on one XCD so concurrently running query tiles stream the same
 // K/V rows through that XCD's L2.
 //
-// Per key tile of 64 cached rows (double-buffered in LDS, the next tile's
-// global loads in flight during the current tile's math):
+// K/V tiles of 64 cached rows go global -> LDS directly (global_load_lds_dwordx4:
+// each wave instruction fills one contiguous 1 KB segment of LDS, lane l at
+// byte 16*l), three tiles deep, issued two tiles ahead, one barrier per tile.
+// Rows are stored unpadded with the 16-byte chunks of each row permuted by an
+// XOR with a function of the row (K: f(r) = ((r&3)<<2)|((r>>2)&3) for 128-wide
+// heads; V: f(r) = (r&3)<<2), so that the K fragment reads (16 rows, one chunk)
+// and the V transpose reads (4 rows, 4 chunks) both hit disjoint LDS banks.
+// Rows beyond N are loaded from row N-1 and masked out of the softmax.
+//
+// Keys are consumed in 32-row blocks. Per block:
 //   S^T = K Q^T - m   v_mfma_f32_32x32x16_bf16 with K rows as the A operand
-//                 straight from LDS and the wave's Q fragments resident in
-//                 VGPRs as the B operand. Q is pre-multiplied by
-//                 scale*log2(e) and the accumulator is seeded (C operand, not
-//                 written) with -m, m the wave's reference maximum in log2
-//                 units, so each score leaves the MFMA ready for exp2. Each
-//                 lane holds 16 scores of ONE query (column l%32) over 32
-//                 keys shared with lane l^32.
+//                 from LDS and the wave's Q fragments resident in VGPRs as
+//                 the B operand. Q is pre-multiplied by scale*log2(e) and the
+//                 accumulator is seeded (C operand, not written) with -m, m the
+//                 wave's reference maximum in log2 units, so each score leaves
+//                 the MFMA ready for exp2. Each lane holds 16 scores of ONE
+//                 query (column l%32) over 32 keys shared with lane l^32.
 //   softmax       the fast path is exp2, a running sum and the bf16 pack per
-//                 score. The reference maximum m is set from the first 32
-//                 keys and only raised (rescaling O and the sum) when some
-//                 probability of a 32-key block exceeds 2^16, detected from
-//                 the block's sum: a wave-uniform branch that is almost never
-//                 taken. Probabilities therefore stay below 2^16 and the sum
-//                 at or above 1.
+//                 score. The reference maximum m is set from the first 32 keys
+//                 and only raised (rescaling O and the sum) when some
+//                 probability of a block exceeds 2^16, detected from the
+//                 block's sum: a wave-uniform branch that is almost never
+//                 taken. Probabilities stay below 2^16 and the sum at or
+//                 above 1.
 //   O^T += V^T P^T  the probabilities, rounded to bf16, are the B operand as
 //                 they sit in the S^T accumulators; the contraction slot
 //                 (hi*8 + e) of each 16-key step maps to key (e/4)*8 + hi*4 +
-//                 e%4. The V^T operand is read from the row-major LDS tile
-//                 with ds_read_b64_tr_b16 (gfx950 LDS transpose read): in each
-//                 16-lane group, lane i points at 4 consecutive channels of
-//                 key row i/4, and lane L receives one channel of 4 keys. The
-//                 V tile row stride is an odd multiple of 16 dwords so the
-//                 eight key rows one read touches fall on disjoint banks.
-//   Every lane owns one query column in both S^T and O^T, so the softmax
-//   statistics never need to be broadcast across lanes.
+//                 e%4. The V^T operand comes from ds_read_b64_tr_b16 (gfx950
+//                 LDS transpose read): in each 16-lane group, lane i points at
+//                 4 consecutive channels of key row i/4, and lane L receives
+//                 one channel of 4 keys.
+// Software pipeline: the S^T MFMAs of block b+1 are issued next to the
+// exp2/sum instructions of block b (they are independent), then the PV MFMAs
+// of block b. Every lane owns one query column in both S^T and O^T, so the
+// softmax statistics never need to be broadcast across lanes.
 #include "common.h"
+
+#include <type_traits>
 
 namespace hsa {
 namespace {
 
 constexpr int BKV = 64;                 // cached rows per LDS tile
+constexpr int NBUF = 3;                 // LDS tiles in flight
 constexpr float kSlowSum = 65536.0f;    // 2^16: raise the reference maximum
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void global_cvoid;
 
-template <int DH, int QT, int NW>
+// s_waitcnt immediate for "vector memory counter <= n", other counters free
+constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+// chunk permutation of cached row r inside a tile (see header)
+template <int DH>
+__device__ __forceinline__ int swz_k(int r) {
+  return DH == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((r >> 1) & 7);
+}
+template <int DH>
+__device__ __forceinline__ int swz_v(int r) {
+  return DH == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
+}
+
+template <int DH, int NW>
 __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
-    bf16* __restrict__ o, int n_q, int n_kv, int d, float sl2e, int n_qtiles, int heads) {
-  constexpr int NT = NW * 64;        // threads
-  constexpr int BQ = NW * 32 * QT;   // queries per workgroup
-  constexpr int KS = DH + 8;         // K tile row stride in bf16 (68 dwords for DH=128)
-  constexpr int VS = DH == 128 ? 160 : 96;  // V tile row stride: 80 / 48 dwords
+    bf16* __restrict__ o, int n_q, int n_kv, int d, float sl2e, int n_qtiles) {
+  constexpr int BQ = NW * 32;        // queries per workgroup
   constexpr int CPR = DH / 8;        // 16-byte chunks per cached row
-  constexpr int LOADS = BKV * CPR / NT;
+  constexpr int RPS = 64 / CPR;      // rows per 1 KB LDS segment
+  constexpr int SEGS = BKV / RPS;    // segments per tile
+  constexpr int LOADS = SEGS / NW;   // segment loads per wave per tensor per tile
   constexpr int DT = DH / 32;        // 32-wide head-dim tiles of O^T
   constexpr int KK = DH / 16;        // k-steps of S^T
-  static_assert(LOADS * NT == BKV * CPR, "tile load must split evenly");
-  __shared__ __attribute__((aligned(16))) bf16 Ks[2][BKV * KS];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[2][BKV * VS];
+  static_assert(LOADS * NW == SEGS, "tile load must split evenly over waves");
+  // one array per buffer: with compile-time buffer indices the compiler can
+  // tell the asynchronous tile loads from the LDS reads of other buffers
+  __shared__ __attribute__((aligned(16))) bf16 K0[BKV * DH], K1[BKV * DH], K2[BKV * DH];
+  __shared__ __attribute__((aligned(16))) bf16 V0[BKV * DH], V1[BKV * DH], V2[BKV * DH];
+  auto kbuf = [&](auto b) -> bf16* {
+    constexpr int B = decltype(b)::value;
+    if constexpr (B == 0) return K0; else if constexpr (B == 1) return K1; else return K2;
+  };
+  auto vbuf = [&](auto b) -> bf16* {
+    constexpr int B = decltype(b)::value;
+    if constexpr (B == 0) return V0; else if constexpr (B == 1) return V1; else return V2;
+  };
 
-  const int item = xcd_contiguous(blockIdx.x, n_qtiles * heads);
+  const int item = xcd_contiguous(blockIdx.x, n_qtiles * (d / DH));
   const int h = item / n_qtiles;
   const int qt = item - h * n_qtiles;
-  const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const long col0 = (long)h * DH;
 
-  // Q fragments, pre-scaled by scale*log2(e): lane holds
-  // Q[query l32 of sub-tile tq][kk*16 + hi*8 + 0..7]
-  bf16x8 qf[QT][KK];
-#pragma unroll
-  for (int tq = 0; tq < QT; ++tq) {
-    const int qrow = qt * BQ + wave * 32 * QT + tq * 32 + l32;
+  // Q fragments, pre-scaled by scale*log2(e): lane holds Q[query l32][kk*16 + hi*8 + 0..7]
+  bf16x8 qf[KK];
+  {
+    const int qrow = qt * BQ + wave * 32 + l32;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       bf16x8 raw = (bf16x8){};
@@ -82,186 +113,186 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
         raw = *reinterpret_cast<const bf16x8*>(q + (long)qrow * d + col0 + kk * 16 + hi * 8);
       f32x4 lo = {(float)raw[0] * sl2e, (float)raw[1] * sl2e, (float)raw[2] * sl2e, (float)raw[3] * sl2e};
       f32x4 up = {(float)raw[4] * sl2e, (float)raw[5] * sl2e, (float)raw[6] * sl2e, (float)raw[7] * sl2e};
-      qf[tq][kk] = __builtin_shufflevector(to_bf16x4(lo), to_bf16x4(up), 0, 1, 2, 3, 4, 5, 6, 7);
+      qf[kk] = __builtin_shufflevector(to_bf16x4(lo), to_bf16x4(up), 0, 1, 2, 3, 4, 5, 6, 7);
     }
   }
 
-  u32x4 rk[LOADS], rv[LOADS];
-  auto gload = [&](int kv0) {
+  // this lane's part of a tile load: segment seg = i*NW + wave, row seg*RPS + lane/CPR,
+  // LDS slot lane%CPR holding global chunk slot ^ f(row)
+  const bf16* kg = kc + col0;
+  const bf16* vg = vc + col0;
+  auto issue_tile = [&](auto buf, int kv0) {
+    bf16* kd = kbuf(buf);
+    bf16* vd = vbuf(buf);
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
-      const int id = t + NT * i;
-      const int row = id / CPR, cc = id % CPR;
-      const int n = kv0 + row;
-      if (n < n_kv) {
-        const long off = (long)n * d + col0 + cc * 8;
-        rk[i] = *reinterpret_cast<const u32x4*>(kc + off);
-        rv[i] = *reinterpret_cast<const u32x4*>(vc + off);
-      } else {
-        rk[i] = (u32x4){0u, 0u, 0u, 0u};
-        rv[i] = (u32x4){0u, 0u, 0u, 0u};
+      const int seg = i * NW + wave;
+      const int row = seg * RPS + lane / CPR;
+      const int slot = lane % CPR;
+      const long n = min(kv0 + row, n_kv - 1);
+      const bf16* ks = kg + n * d + (slot ^ swz_k<DH>(row)) * 8;
+      const bf16* vs = vg + n * d + (slot ^ swz_v<DH>(row)) * 8;
+      __builtin_amdgcn_global_load_lds((global_cvoid*)ks, (lds_void*)(kd + seg * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((global_cvoid*)vs, (lds_void*)(vd + seg * 512), 16, 0, 0);
+    }
+  };
+
+  // LDS element offsets this lane reads, relative to a 32-key block
+  int koff[KK];  // K fragment kk: row l32, chunk kk*2 + hi
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) koff[kk] = l32 * DH + (((kk * 2 + hi) ^ swz_k<DH>(l32)) * 8);
+  int voff[DT];  // V transpose read, head-dim tile dt: row hi*4 + k, channel dt*32 + 16g + 4(lane&3)
+  {
+    const int k4 = (lane & 15) >> 2, g = (lane >> 4) & 1;
+    const int r = hi * 4 + k4;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int col = dt * 32 + 16 * g + 4 * (lane & 3);
+      voff[dt] = r * DH + (((col >> 3) ^ swz_v<DH>(r)) * 8) + (col & 7);
+    }
+  }
+
+  f32x16 acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) acc[dt] = (f32x16){};
+  f32x16 negm = (f32x16){};  // every element -m_ref: the seed of the score accumulators
+  float m_ref = 0.f, l_run = 0.f;
+  bool have_ref = false;     // becomes true after the first 32 keys (wave-uniform)
+
+  // S^T of the 32-key block starting at row kb of tile buffer buf
+  auto scores = [&](auto buf, int kb, f32x16& s) {
+    const bf16* base = kbuf(buf) + kb * DH;
+    bf16x8 kf[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) kf[kk] = *reinterpret_cast<const bf16x8*>(base + koff[kk]);
+    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[0], negm, 0, 0, 0);
+#pragma unroll
+    for (int kk = 1; kk < KK; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], s, 0, 0, 0);
+  };
+
+  // One pipeline step: issue S^T of the next block, softmax of the current
+  // block (keys key0 .. key0+31, V rows vb .. vb+31 of buffer buf), PV. The
+  // next block's scores are always computed from a valid LDS address so that
+  // they share a scheduling region with the softmax; after the last block
+  // they are unused.
+  auto step = [&](f32x16& s_cur, f32x16& s_nxt, auto nbuf, int nkb, auto buf, int vb, int key0) {
+    if (key0 + 32 > n_kv) {  // ragged last block: mask the keys beyond N
+      const int kbase = key0 + hi * 4;
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (kbase + (e >> 2) * 8 + (e & 3) >= n_kv) s_cur[e] = -INFINITY;
+    }
+    scores(nbuf, nkb, s_nxt);
+    float p[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(s_cur[e]);
+    float ls = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7])) +
+               (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
+    if (__any(!have_ref || !(ls <= kSlowSum))) {
+      // set or raise the reference maximum, rescale what was accumulated
+      float mx = s_cur[0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s_cur[e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));               // block max relative to m_ref
+      const float up = have_ref ? fmaxf(mx, 0.f) : mx;  // amount to raise m_ref by
+      const float alpha = have_ref ? __builtin_amdgcn_exp2f(-up) : 0.f;
+      ls = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(s_cur[e] - up);
+        ls += p[e];
+      }
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[dt] *= alpha;
+      m_ref += up;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        negm[e] = -m_ref;
+        s_nxt[e] -= up;  // the next block's scores were seeded with the old reference
+      }
+      have_ref = true;
+    }
+    l_run += ls;
+    bf16x8 pf[2];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      f32x4 lo = {p[8 * half + 0], p[8 * half + 1], p[8 * half + 2], p[8 * half + 3]};
+      f32x4 up = {p[8 * half + 4], p[8 * half + 5], p[8 * half + 6], p[8 * half + 7]};
+      pf[half] = __builtin_shufflevector(to_bf16x4(lo), to_bf16x4(up), 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    const bf16* vbase = vbuf(buf) + vb * DH;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16* src = vbase + ks * 16 * DH + voff[dt];
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src + 8 * DH));
+        const bf16x8 vf = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], acc[dt], 0, 0, 0);
       }
     }
   };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int id = t + NT * i;
-      const int row = id / CPR, cc = id % CPR;
-      *reinterpret_cast<u32x4*>(&Ks[buf][row * KS + cc * 8]) = rk[i];
-      *reinterpret_cast<u32x4*>(&Vs[buf][row * VS + cc * 8]) = rv[i];
-    }
-  };
 
-  // transpose-read source of this lane inside a 16-key step (see header)
-  const int v_lane = (hi * 4 + ((lane & 15) >> 2)) * VS + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int k_lane = l32 * KS + hi * 8;
-
-  f32x16 acc[QT][DT];
-  f32x16 negm[QT];  // every element -m_ref: the seed of the score accumulators
-  float m_ref[QT], l_run[QT];
-#pragma unroll
-  for (int tq = 0; tq < QT; ++tq) {
-    m_ref[tq] = 0.f;
-    l_run[tq] = 0.f;
-    negm[tq] = (f32x16){};
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) acc[tq][dt] = (f32x16){};
-  }
-  bool have_ref = false;  // becomes true after the first 32 keys (wave-uniform)
-
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using B2 = std::integral_constant<int, 2>;
   const int n_tiles = (n_kv + BKV - 1) / BKV;
-  gload(0);
-  lstore(0);
+  issue_tile(B0{}, 0);
+  if (n_tiles > 1) issue_tile(B1{}, BKV);
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();
-  for (int it = 0; it < n_tiles; ++it) {
-    const int buf = it & 1;
+  f32x16 sa, sb;
+  scores(B0{}, 0, sa);
+  // tile it lives in buffer it % 3; the loop is unrolled by 3 so that every
+  // buffer index is a compile-time constant
+  auto tile = [&](auto buf, auto nxt, auto nn, int it) {
     const int kv0 = it * BKV;
-    if (it + 1 < n_tiles) gload(kv0 + BKV);
-    const bf16* Kt = Ks[buf];
-    const bf16* Vt = Vs[buf];
-#pragma unroll
-    for (int sb = 0; sb < BKV / 32; ++sb) {
-      f32x16 s[QT];
-      {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kt[sb * 32 * KS + k_lane]);
-#pragma unroll
-        for (int tq = 0; tq < QT; ++tq)
-          s[tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[tq][0], negm[tq], 0, 0, 0);
-      }
-#pragma unroll
-      for (int kk = 1; kk < KK; ++kk) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kt[sb * 32 * KS + k_lane + kk * 16]);
-#pragma unroll
-        for (int tq = 0; tq < QT; ++tq)
-          s[tq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[tq][kk], s[tq], 0, 0, 0);
-      }
-      // s[tq][e] = scaled score of key kv0 + sb*32 + (e/4)*8 + hi*4 + e%4, minus m_ref
-      if (kv0 + sb * 32 + 32 > n_kv) {
-        const int key0 = kv0 + sb * 32 + hi * 4;
-#pragma unroll
-        for (int tq = 0; tq < QT; ++tq)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (key0 + (e >> 2) * 8 + (e & 3) >= n_kv) s[tq][e] = -INFINITY;
-      }
-      bf16x8 pf[QT][2];
-      float p[QT][16];
-      float ls[QT];
-      bool slow = !have_ref;
-#pragma unroll
-      for (int tq = 0; tq < QT; ++tq) {
-        ls[tq] = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          p[tq][e] = __builtin_amdgcn_exp2f(s[tq][e]);
-          ls[tq] += p[tq][e];
-        }
-        slow |= !(ls[tq] <= kSlowSum);
-      }
-      if (__any(slow)) {
-        // set or raise the reference maximum, rescale what was accumulated
-#pragma unroll
-        for (int tq = 0; tq < QT; ++tq) {
-          float mx = s[tq][0];
-#pragma unroll
-          for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[tq][e]);
-          mx = fmaxf(mx, __shfl_xor(mx, 32));            // block max relative to m_ref
-          const float up = have_ref ? fmaxf(mx, 0.f) : mx;  // amount to raise m_ref by
-          const float alpha = have_ref ? __builtin_amdgcn_exp2f(-up) : 0.f;
-          ls[tq] = 0.f;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            p[tq][e] = __builtin_amdgcn_exp2f(s[tq][e] - up);
-            ls[tq] += p[tq][e];
-          }
-          l_run[tq] *= alpha;
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) acc[tq][dt] *= alpha;
-          m_ref[tq] += up;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) negm[tq][e] = -m_ref[tq];
-        }
-        have_ref = true;
-      }
-#pragma unroll
-      for (int tq = 0; tq < QT; ++tq) {
-        l_run[tq] += ls[tq];
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          f32x4 lo = {p[tq][8 * half + 0], p[tq][8 * half + 1], p[tq][8 * half + 2], p[tq][8 * half + 3]};
-          f32x4 up = {p[tq][8 * half + 4], p[tq][8 * half + 5], p[tq][8 * half + 6], p[tq][8 * half + 7]};
-          pf[tq][half] = __builtin_shufflevector(to_bf16x4(lo), to_bf16x4(up), 0, 1, 2, 3, 4, 5, 6, 7);
-        }
-      }
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const bf16* vb = Vt + (sb * 32 + ks * 16) * VS + dt * 32 + v_lane;
-          const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vb));
-          const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vb + 8 * VS));
-          const bf16x8 vf = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-          for (int tq = 0; tq < QT; ++tq)
-            acc[tq][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[tq][ks], acc[tq][dt], 0, 0, 0);
-        }
-      }
-    }
-    if (it + 1 < n_tiles) lstore(buf ^ 1);
+    // block 0 of this tile; the next block is block 1 of the same tile
+    step(sa, sb, buf, 32, buf, 0, kv0);
+    // tile it+1 (issued one iteration ago) has landed; after this barrier every
+    // wave is done with tile it-1, whose buffer receives tile it+2
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
+    if (it + 2 < n_tiles) issue_tile(nn, kv0 + 2 * BKV);
+    // block 1 of this tile; the next block is block 0 of tile it+1
+    if (kv0 + 32 < n_kv) step(sb, sa, nxt, 0, buf, 32, kv0 + 32);
+  };
+  for (int it = 0; it < n_tiles; it += NBUF) {
+    tile(B0{}, B1{}, B2{}, it);
+    if (it + 1 < n_tiles) tile(B1{}, B2{}, B0{}, it + 1);
+    if (it + 2 < n_tiles) tile(B2{}, B0{}, B1{}, it + 2);
   }
 
-  // acc[tq][dt][e]: channel dt*32 + (e/4)*8 + hi*4 + e%4 of query l32
-#pragma unroll
-  for (int tq = 0; tq < QT; ++tq) {
-    const float l_tot = l_run[tq] + __shfl_xor(l_run[tq], 32);
-    const float inv = 1.f / l_tot;
-    const int qrow = qt * BQ + wave * 32 * QT + tq * 32 + l32;
-    if (qrow >= n_q) continue;
+  // acc[dt][e]: channel dt*32 + (e/4)*8 + hi*4 + e%4 of query l32
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv = 1.f / l_tot;
+  const int qrow = qt * BQ + wave * 32 + l32;
+  if (qrow < n_q) {
     bf16* dst = o + (long)qrow * d + col0;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        f32x4 v = {acc[tq][dt][4 * g + 0] * inv, acc[tq][dt][4 * g + 1] * inv,
-                   acc[tq][dt][4 * g + 2] * inv, acc[tq][dt][4 * g + 3] * inv};
+        f32x4 v = {acc[dt][4 * g + 0] * inv, acc[dt][4 * g + 1] * inv, acc[dt][4 * g + 2] * inv,
+                   acc[dt][4 * g + 3] * inv};
         *reinterpret_cast<bf16x4*>(dst + dt * 32 + g * 8 + hi * 4) = to_bf16x4(v);
       }
     }
   }
 }
 
-template <int DH, int QT, int NW>
+template <int DH, int NW>
 hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
                       int heads, float sl2e, hipStream_t s) {
-  constexpr int BQ = NW * 32 * QT;
+  constexpr int BQ = NW * 32;
   const int n_qtiles = (n_q + BQ - 1) / BQ;
   const int d = heads * DH;
-  hipLaunchKernelGGL((attention_bf16_kernel<DH, QT, NW>), dim3((unsigned)(n_qtiles * heads)),
+  hipLaunchKernelGGL((attention_bf16_kernel<DH, NW>), dim3((unsigned)(n_qtiles * heads)),
                      dim3(NW * 64), 0, s, static_cast<const bf16*>(q),
                      static_cast<const bf16*>(k), static_cast<const bf16*>(v),
-                     static_cast<bf16*>(o), n_q, n_kv, d, sl2e, n_qtiles, heads);
+                     static_cast<bf16*>(o), n_q, n_kv, d, sl2e, n_qtiles);
   return hipGetLastError();
 }
 
@@ -271,28 +302,17 @@ hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, vo
                                  int n_kv, int heads, int head_dim, float scale, hipStream_t s) {
   if (n_q <= 0) return hipSuccess;
   const float sl2e = scale * 1.4426950408889634f;
-  // Workgroup shape: 8 waves x 32 queries (two waves per SIMD, so one wave's
-  // softmax overlaps the other's MFMAs) whenever that still gives every CU a
-  // workgroup; 4 waves x 32 queries for small problems. HSA_ATTN_CFG (1, 2, 3)
-  // forces a shape for measurement sweeps.
-  static const int forced = [] {
-    const char* e = getenv("HSA_ATTN_CFG");
-    return e ? atoi(e) : 0;
-  }();
-  int cfg = forced;
-  if (cfg < 1 || cfg > 3) cfg = ((long)((n_q + 255) / 256) * heads >= 256) ? 3 : 1;
-  if (head_dim == 64) {
-    switch (cfg) {
-      case 2: return launch_cfg<64, 2, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-      case 3: return launch_cfg<64, 1, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-      default: return launch_cfg<64, 1, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-    }
-  }
-  switch (cfg) {
-    case 2: return launch_cfg<128, 2, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-    case 3: return launch_cfg<128, 1, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-    default: return launch_cfg<128, 1, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-  }
+  // Workgroup shape: 8 waves (two per SIMD, 256 queries) whenever that still
+  // gives every CU a workgroup, else 4 waves (128 queries). HSA_ATTN_WAVES
+  // (4 or 8) forces a shape for measurement sweeps.
+  const char* forced = getenv("HSA_ATTN_WAVES");
+  int nw = forced ? atoi(forced) : 0;
+  if (nw != 4 && nw != 8) nw = ((long)((n_q + 255) / 256) * heads >= 256) ? 8 : 4;
+  if (head_dim == 64)
+    return nw == 8 ? launch_cfg<64, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s)
+                   : launch_cfg<64, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
+  return nw == 8 ? launch_cfg<128, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s)
+                 : launch_cfg<128, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
 }
 
 }  // namespace hsa

@@ -285,15 +285,15 @@ def test_active_attention_equals_core_then_projection():
     assert torch.equal(ws.view(nA, d), o)
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3])
+@pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("dh", [64, 128])
-def test_attention_every_tile_config(cfg, dh, monkeypatch):
-    """Each workgroup shape the launcher can pick (1: 4 waves x 32 queries,
-    2: 4 waves x 64 queries, 3: 8 waves x 32 queries) on ragged sizes."""
-    monkeypatch.setenv("HSA_ATTN_CFG", str(cfg))
+def test_attention_every_tile_config(waves, dh, monkeypatch):
+    """Each workgroup shape the launcher can pick (4 or 8 waves of 32 queries)
+    on ragged sizes."""
+    monkeypatch.setenv("HSA_ATTN_WAVES", str(waves))
     N, nA, heads = 1111, 777, 3
     d = heads * dh
-    rng = np.random.default_rng(cfg * 1000 + dh)
+    rng = np.random.default_rng(waves * 1000 + dh)
     q_np, k_np, v_np = (synth.to_bf16_values(rng.standard_normal((r, d)).astype(np.float32)) for r in (nA, N, N))
     scale = 1.0 / math.sqrt(dh)
     o = torch.empty(nA, d, dtype=torch.bfloat16, device=DEV)
