@@ -8,31 +8,54 @@
 //     tokens fused into the epilogue.
 // The compact gathered activations are never materialized in HBM.
 //
-// Tiling: 128 x 128 output tile per 256-thread workgroup (4 waves in 2 x 2,
-// 64 x 64 per wave = 2 x 2 tiles of v_mfma_f32_32x32x16_bf16), K step 64,
-// two LDS buffers (global loads of step k+1 overlap the MFMAs of step k).
+// Tiling: BM x BN output tile per 512-thread workgroup (8 waves in a WM x WN
+// grid), K step 64, v_mfma_f32_32x32x16_bf16. Tiles go global -> LDS directly
+// (global_load_lds_dwordx4: one wave instruction fills one contiguous 1 KB
+// segment = 8 tile rows of 128 bytes) into two stages, the loads of step k+1
+// in flight during the MFMAs of step k, one barrier per step. The 16-byte
+// chunks of tile row r sit at slot chunk ^ ((r >> 1) & 7), which keeps the
+// fragment reads (16 rows, one chunk) on disjoint banks. Each stage is its own
+// LDS array and the K loop is unrolled by 2, so the compiler can tell the
+// asynchronous loads from reads of the other stage.
 // Every tile row is a contiguous 128-byte run of a token row, so the indexed
-// loads stay coalesced. The product is formed transposed (B rows drive the
+// loads stay coalesced; rows outside the problem are read from a valid row and
+// their results dropped. The product is formed transposed (B rows drive the
 // MFMA A operand), which leaves each lane holding one output row and runs of
 // four consecutive columns: one row-index lookup per lane and 8-byte stores.
 // Tiles are ordered in groups of 8 tile-rows and laid out contiguously per XCD
 // so the A and B panels a group shares stay in that XCD's L2.
 #include "common.h"
 
+#include <type_traits>
+
 namespace hsa {
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64, kThreads = 256;
-constexpr int LS = BK + 8;  // LDS row stride in bf16 (144 bytes, 16-byte aligned)
+constexpr int BK = 64, kWaves = 8, kThreads = kWaves * 64;
 constexpr int kGroupM = 8;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void global_cvoid;
+
+constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 // NOUT (1 or 3) is the number of outputs sharing A; it is a template
 // parameter so the Q/K/V projection and the output projection are distinct
 // kernels in profiles.
-template <int NOUT>
-__global__ __launch_bounds__(kThreads, 2) void row_gemm_bf16_kernel(RowGemm g) {
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LS];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LS];
+template <int BM, int BN, int WM, int NOUT>
+__global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
+  constexpr int WN = kWaves / WM;
+  constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
+  constexpr int MI = TM / 32, NI = TN / 32;  // 32x32 MFMA tiles per wave
+  constexpr int SEG_A = BM / 8, SEG_B = BN / 8;  // 1 KB segments per stage
+  constexpr int LOADS = (SEG_A + SEG_B) / kWaves;
+  static_assert(LOADS * kWaves == SEG_A + SEG_B, "stage load must split evenly over waves");
+  __shared__ __attribute__((aligned(16))) bf16 A0[BM * BK], A1[BM * BK];
+  __shared__ __attribute__((aligned(16))) bf16 B0[BN * BK], B1[BN * BK];
+  auto abuf = [&](auto s) -> bf16* { if constexpr (decltype(s)::value == 0) return A0; else return A1; };
+  auto bbuf = [&](auto s) -> bf16* { if constexpr (decltype(s)::value == 0) return B0; else return B1; };
 
   const int tiles_m = (g.M + BM - 1) / BM;
   const int tiles_n1 = (g.Nc + BN - 1) / BN;  // per output
@@ -53,77 +76,87 @@ __global__ __launch_bounds__(kThreads, 2) void row_gemm_bf16_kernel(RowGemm g) {
   const bf16* __restrict__ A = static_cast<const bf16*>(g.A);
   const bf16* __restrict__ B = static_cast<const bf16*>(oz.B);
 
-  const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
   const int l32 = lane & 31, hi = lane >> 5;
 
-  // global -> LDS mapping: 8 threads per 64-element row segment, 4 rows per thread
-  const int lr = t >> 3;
-  const int lc = (t & 7) * 8;
-  const bf16* a_src[4];
-  const bf16* b_src[4];
-  bool a_ok[4], b_ok[4];
+  // This lane's rows of the stage loads: segment s = i*8 + wave covers tile
+  // rows 8s .. 8s+7 (A tile first, then B tile); the lane fetches row
+  // 8s + lane/8, global chunk (lane%8) ^ swz(row) into LDS slot lane%8.
+  const bf16* src[LOADS];
+  int dst[LOADS];  // element offset of the segment in its tile
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = tm * BM + lr + 32 * i;
-    int row = -1;
-    if (m < g.M) row = g.a_rows ? g.a_rows[m] : m;
-    a_ok[i] = row >= 0 && row < g.a_limit;
-    a_src[i] = A + (long)(a_ok[i] ? row : 0) * g.lda + lc;
-    const int n = tn * BN + lr + 32 * i;
-    b_ok[i] = n < g.Nc;
-    b_src[i] = B + (long)(b_ok[i] ? n : 0) * g.ldb + lc;
+  for (int i = 0; i < LOADS; ++i) {
+    const int s = i * kWaves + wave;
+    const bool a = s < SEG_A;
+    const int trow = (a ? s : s - SEG_A) * 8 + lane / 8;
+    const int chunk = (lane % 8) ^ swz(trow);
+    long grow;
+    if (a) {
+      const int m = tm * BM + trow;
+      int row = (m < g.M) ? (g.a_rows ? g.a_rows[m] : m) : 0;
+      if (row < 0 || row >= g.a_limit) row = 0;
+      grow = (long)row * g.lda;
+    } else {
+      const int n = min(tn * BN + trow, g.Nc - 1);
+      grow = (long)n * g.ldb;
+    }
+    src[i] = (a ? A : B) + grow + chunk * 8;
+    dst[i] = (a ? s : s - SEG_A) * 512;
   }
-
-  u32x4 ra[4], rb[4];
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  auto gload = [&](int k0) {
+  auto issue = [&](auto st, int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = a_ok[i] ? *reinterpret_cast<const u32x4*>(a_src[i] + k0) : zero;
-      rb[i] = b_ok[i] ? *reinterpret_cast<const u32x4*>(b_src[i] + k0) : zero;
+    for (int i = 0; i < LOADS; ++i) {
+      // segments i*8 + wave: all of one wave's segments of load i lie in the
+      // same tile when SEG_A is a multiple of 8 (always true here)
+      bf16* base = (i * kWaves < SEG_A) ? abuf(st) : bbuf(st);
+      __builtin_amdgcn_global_load_lds((global_cvoid*)(src[i] + k0), (lds_void*)(base + dst[i]), 16, 0, 0);
     }
   };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<u32x4*>(&As[buf][(lr + 32 * i) * LS + lc]) = ra[i];
-      *reinterpret_cast<u32x4*>(&Bs[buf][(lr + 32 * i) * LS + lc]) = rb[i];
-    }
-  };
+  static_assert(SEG_A % kWaves == 0, "A segments must fill whole load rounds");
 
-  f32x16 acc[2][2];
+  // fragment read offsets: row (tile-local) l32 + 32*t, chunk kk*2 + hi
+  const int xr = ((hi ^ swz(l32)) * 8);  // chunk kk*2+hi ^ f = (kk*2) ^ (hi ^ f); f(r) = f(r % 16)
+  f32x16 acc[MI][NI];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16){};
+    for (int j = 0; j < NI; ++j) acc[i][j] = (f32x16){};
 
-  const int nk = g.K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+  auto compute = [&](auto st) {
+    const bf16* As = abuf(st) + (wm * TM + l32) * BK;
+    const bf16* Bs = bbuf(st) + (wn * TN + l32) * BK;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[2], bfr[2];
+      const int off = (kk * 16) ^ xr;
+      bf16x8 af[MI], bfr[NI];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        af[i] = *reinterpret_cast<const bf16x8*>(
-            &As[buf][(wm * 64 + i * 32 + l32) * LS + kk * 16 + hi * 8]);
-        bfr[i] = *reinterpret_cast<const bf16x8*>(
-            &Bs[buf][(wn * 64 + i * 32 + l32) * LS + kk * 16 + hi * 8]);
-      }
+      for (int i = 0; i < MI; ++i) af[i] = *reinterpret_cast<const bf16x8*>(As + i * 32 * BK + off);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < NI; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * BK + off);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
+  };
+
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  const int nk = g.K / BK;
+  issue(S0{}, 0);
+  // step k lives in stage k % 2: wait for its loads, make them visible (and
+  // free the other stage), start step k+1's loads, compute step k
+  auto step = [&](auto st, auto other, int k) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
+    if (k + 1 < nk) issue(other, (k + 1) * BK);
+    compute(st);
+  };
+  for (int k = 0; k < nk; k += 2) {
+    step(S0{}, S1{}, k);
+    if (k + 1 < nk) step(S1{}, S0{}, k + 1);
   }
 
   // acc[i][j][e]: output row m = tile row + i*32 + l32,
@@ -131,37 +164,44 @@ __global__ __launch_bounds__(kThreads, 2) void row_gemm_bf16_kernel(RowGemm g) {
   bf16* __restrict__ C = static_cast<bf16*>(oz.C);
   const int32_t* c_rows = oz.c_rows;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int m = tm * BM + wm * 64 + i * 32 + l32;
+  for (int i = 0; i < MI; ++i) {
+    const int m = tm * BM + wm * TM + i * 32 + l32;
     if (m >= g.M) continue;
     const int crow = c_rows ? c_rows[m] : m;
     if (crow < 0 || crow >= oz.c_limit) continue;
-    bf16* dst = C + (long)crow * g.ldc;
+    bf16* out = C + (long)crow * g.ldc;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < NI; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int n = tn * BN + wn * 64 + j * 32 + q * 8 + hi * 4;
+        const int n = tn * BN + wn * TN + j * 32 + q * 8 + hi * 4;
         if (n < g.Nc) {
           f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                      acc[i][j][4 * q + 3]};
-          *reinterpret_cast<bf16x4*>(dst + n) = to_bf16x4(v);
+          *reinterpret_cast<bf16x4*>(out + n) = to_bf16x4(v);
         }
       }
     }
   }
 }
 
+template <int BM, int BN, int WM, int NOUT>
+hipError_t launch(const RowGemm& g, hipStream_t s) {
+  const long tiles = (long)((g.M + BM - 1) / BM) * ((g.Nc + BN - 1) / BN) * NOUT;
+  hipLaunchKernelGGL((row_gemm_bf16_kernel<BM, BN, WM, NOUT>), dim3((unsigned)tiles),
+                     dim3(kThreads), 0, s, g);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.Nc <= 0 || (g.n_out != 1 && g.n_out != 3)) return hipSuccess;
-  const long tiles = (long)((g.M + BM - 1) / BM) * ((g.Nc + BN - 1) / BN) * g.n_out;
-  if (g.n_out == 3)
-    hipLaunchKernelGGL(row_gemm_bf16_kernel<3>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
-  else
-    hipLaunchKernelGGL(row_gemm_bf16_kernel<1>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
-  return hipGetLastError();
+  // 256 x 256 tiles (8 waves of 128 x 64) for the three-output projection;
+  // 256 x 128 tiles (8 waves of 64 x 64) for the single-output one, whose grid
+  // would otherwise leave CUs idle in the last round of workgroups.
+  if (g.n_out == 3) return launch<256, 256, 2, 3>(g, s);
+  return launch<256, 128, 4, 1>(g, s);
 }
 
 }  // namespace hsa
