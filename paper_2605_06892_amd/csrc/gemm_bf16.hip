@@ -9,7 +9,9 @@
 // The compact gathered activations are never materialized in HBM.
 //
 // Tiling: BM x BN output tile per 512-thread workgroup (8 waves in a WM x WN
-// grid), K step 64, v_mfma_f32_32x32x16_bf16. Tiles go global -> LDS directly
+// grid), K step 64, v_mfma_f32_32x32x16_bf16; the fragments of the next
+// 16-wide k slice are read from LDS while the MFMAs of the current one run.
+// Tiles go global -> LDS directly
 // (global_load_lds_dwordx4: one wave instruction fills one contiguous 1 KB
 // segment = 8 tile rows of 128 bytes) into two stages, the loads of step k+1
 // in flight during the MFMAs of step k, one barrier per step. The 16-byte
@@ -126,19 +128,27 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
   auto compute = [&](auto st) {
     const bf16* As = abuf(st) + (wm * TM + l32) * BK;
     const bf16* Bs = bbuf(st) + (wn * TN + l32) * BK;
+    bf16x8 af[2][MI], bfr[2][NI];
+    auto ld = [&](int kk, int b) {
+      const int off = (kk * 16) ^ xr;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) af[b][i] = *reinterpret_cast<const bf16x8*>(As + i * 32 * BK + off);
+#pragma unroll
+      for (int j = 0; j < NI; ++j) bfr[b][j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * BK + off);
+    };
+    ld(0, 0);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int off = (kk * 16) ^ xr;
-      bf16x8 af[MI], bfr[NI];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) af[i] = *reinterpret_cast<const bf16x8*>(As + i * 32 * BK + off);
-#pragma unroll
-      for (int j = 0; j < NI; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * BK + off);
+      if (kk + 1 < BK / 16) ld(kk + 1, (kk + 1) & 1);
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i], acc[i][j], 0, 0, 0);
+      if (kk + 1 < BK / 16) {
+        __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, MI * NI, 0);
+      }
     }
   };
 
