@@ -57,6 +57,8 @@ def parse():
     p.add_argument("--second-iteration", type=int, default=2, help="also time this iteration (-1: skip)")
     p.add_argument("--layout", default="scattered", choices=["scattered", "contiguous"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-schedules", action="store_true", help="skip the preset-schedule trajectories")
+    p.add_argument("--no-euler-stress", action="store_true", help="skip the Euler bandwidth-stress shape")
     p.add_argument("--summarize", metavar="DIR", default=None,
                    help="print a text summary of the rocprofv3 csv output under DIR and exit")
     p.add_argument("--write-traffic", metavar="DIR", default=None,
@@ -91,14 +93,14 @@ def setup(wl, layout, dev):
     return blk, budget, b, eul
 
 
-def run_step(b, eul, T, it, sigmas, ev=None):
+def run_step(b, eul, T, it, sigmas, ev=None, margin=0):
     """One full pass of the hot path; if ev is given, record events between calls."""
     from paper_2605_06892_amd import hsa_step as H
     from paper_2605_06892_amd import layer as L
 
     rec = (lambda k: ev[k].record()) if ev is not None else (lambda k: None)  # noqa: E731
     rec(0)
-    n = L.active_set(b, T, it)
+    n = L.active_set(b, T, it, margin)
     rec(1)
     L.qkv(b, n)
     rec(2)
@@ -250,6 +252,75 @@ def write_traffic(d):
     return text
 
 
+def schedule_runtimes(dev, name="wan1.3b"):
+    """Wall time of a whole T = 40 sampling trajectory of one layer (active set,
+    layer step, cached Euler update at every iteration) for each budget preset
+    of the paper's Appendix C, relative to the uniform schedule (every token at
+    every iteration, FM with T = 40). Presets with strategy D use the
+    velocity-norm ranking stand-in; HSA-25 uses random allocation (R)."""
+    import torch
+
+    import synth
+    from paper_2605_06892_amd import layer as L
+
+    wl = synth.WORKLOADS[name]
+    blk, _, b, eul = setup(wl, "scattered", dev)
+    T = 40
+    sig = synth.linear_sigmas(T)
+
+    def trajectory(budget, margin):
+        b.budget.copy_(torch.from_numpy(budget))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        steps = 0
+        for i in range(T):
+            steps += run_step(b, eul, T, i, sig, margin=margin)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3, steps / (wl.N * T)
+
+    full = np.full(wl.N, T, dtype=np.int32)
+    trajectory(full, 0)  # warm-up
+    fm_ms, _ = trajectory(full, 0)
+    out = {"workload": f"{name} single layer, N={wl.N}, d={wl.d}, T={T}", "fm_T40_ms": round(fm_ms, 2)}
+    for pname, pre in synth.PRESETS.items():
+        layout = "random" if pre["strategy"] == "R" else "scattered"
+        budget = synth.assign_budgets(blk["v_group"], pre["groups"], layout)
+        ms, frac = trajectory(budget, L.window_margin(pre["window"], T))
+        out[pname] = {"ms": round(ms, 2), "runtime_vs_fm": round(ms / fm_ms, 4),
+                      "token_step_fraction": round(frac, 4), "paper_runtime": pre["printed_runtime"]}
+    return out
+
+
+def euler_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
+    """The cached Euler update at a bandwidth-stress shape (16M tokens x 16 fp32
+    channels, every 4th token fresh), far above the 256 MB last-level cache:
+    HBM bytes moved per launch over its event time, against the HBM peak."""
+    import torch
+
+    from paper_2605_06892_amd import hsa_step as H
+
+    x = torch.zeros(n_tokens, channels, device=dev)
+    vc = torch.ones(n_tokens, channels, device=dev)
+    idx = torch.arange(0, n_tokens, 4, dtype=torch.int32, device=dev)
+    na = idx.numel()
+    vf = torch.ones(na, channels, device=dev)
+    ts = []
+    for r in range(reps + 2):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        H.hsa_cached_euler(x, vc, vf, idx, na, 0.5, 0.25)
+        b.record()
+        torch.cuda.synchronize()
+        if r >= 2:
+            ts.append(a.elapsed_time(b))
+    ms = float(np.median(ts))
+    nbytes = n_tokens * channels * 4 * 3 + na * (channels * 4 * 2 + 4)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del x, vc, vf, idx
+    return {"tokens": n_tokens, "channels": channels, "fresh_rows": na, "ms": round(ms, 4),
+            "bytes": nbytes, "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def cpu_baseline(wl, blk, budget, it):
     """The oracle's layer step timed on this host: two bounded samples of the
     active rows (projections, attention against the whole N-row cache, output
@@ -390,6 +461,12 @@ def main():
             "kernels_ms": {k: round(v, 4) for k, v in per2.items()},
             "active_attention_tflops": round(attention_flops(n2, wl.N, wl.d) / (per2["attention"] * 1e-3) / 1e12, 2),
         }
+    if not args.no_euler_stress:
+        out["euler_stress"] = euler_stress(dev)
+    if not args.no_schedules:
+        del b, eul
+        torch.cuda.empty_cache()
+        out["schedules"] = schedule_runtimes(dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, blk, budget, args.iteration)
     print(json.dumps(out))

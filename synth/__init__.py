@@ -7,6 +7,7 @@ oracle and the GPU path consume what it produces.
 """
 
 from .workloads import (  # noqa: F401
+    PRESETS,
     WORKLOADS,
     Workload,
     assign_budgets,

@@ -86,6 +86,21 @@ WORKLOADS = {
 }
 
 
+# Budget presets of the paper's Appendix C (runtimes also in Table 1): token
+# percentages per step budget, the centred caching window (percent of the
+# trajectory) and the token allocation strategy, with T = 40.
+PRESETS = {
+    "HSA-75A": {"T": 40, "groups": ((40, 0.25), (20, 0.25), (10, 0.50)), "window": 50, "strategy": "D",
+                "printed_runtime": 0.75},
+    "HSA-75B": {"T": 40, "groups": ((40, 0.33), (10, 0.67)), "window": 50, "strategy": "D",
+                "printed_runtime": 0.75},
+    "HSA-50": {"T": 40, "groups": ((40, 0.16), (10, 0.84)), "window": 80, "strategy": "D",
+               "printed_runtime": 0.50},
+    "HSA-25": {"T": 40, "groups": ((20, 0.16), (5, 0.84)), "window": 80, "strategy": "R",
+               "printed_runtime": 0.25},
+}
+
+
 def to_bf16_values(a: np.ndarray) -> np.ndarray:
     """Round a float32 array to bf16 (torch's nearest-even conversion) and return
     the rounded values as float32."""
@@ -140,6 +155,8 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
     gets the smallest budget and the highest-norm block the largest.
     layout "contiguous": consecutive index ranges in ascending budget order,
     the largest budget last (the reordered sequence of Section 2.5).
+    layout "random": a seeded random permutation of the tokens (strategy R of
+    Appendix B), seeded from the v_group values.
     """
     N = v_group.shape[0]
     order_groups = sorted(groups, key=lambda g: g[0])  # ascending budget
@@ -152,6 +169,9 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
         rank = np.argsort(norms, kind="stable")
     elif layout == "contiguous":
         rank = np.arange(N)
+    elif layout == "random":
+        seed = int(np.frombuffer(np.ascontiguousarray(v_group[:1], np.float32).tobytes(), np.uint32)[0])
+        rank = np.random.default_rng(seed).permutation(N)
     else:
         raise ValueError(f"unknown layout {layout!r}")
     budget = np.empty(N, dtype=np.int32)
