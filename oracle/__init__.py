@@ -22,3 +22,17 @@ from .hsa_oracle import (  # noqa: F401
     trajectory,
     window_margin,
 )
+from .stack_oracle import (  # noqa: F401
+    assign_groups,
+    boundary_gaps,
+    check_group_sizes,
+    gather_latent,
+    initial_state,
+    linear,
+    refresh_period,
+    stack_forward,
+    stack_iteration,
+    stack_trajectory,
+    token_ranks,
+    velocity_keys,
+)

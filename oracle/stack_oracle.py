@@ -1,0 +1,225 @@
+"""Plain CPU oracle for the multi-layer HSA sampling loop.
+
+TEST INFRASTRUCTURE ONLY, like the rest of this package: imported by the
+tests, the package smoke check and the benchmark's CPU-baseline leg, never by
+the product path, and sharing no code with the HIP library.
+
+It extends the single-block oracle to a stack of L self-attention layers
+driven by the HSA schedule, float64 throughout with one rounding to the
+storage dtype wherever a value is materialized.
+
+What it follows, by section of the paper:
+  * Section 2.3 -- every self-attention layer l keeps its own cache
+    K_hat^(l), V_hat^(l) over all N tokens, written at the first iteration;
+    at iteration i only the rows A_i are recomputed and overwritten, every
+    active query attends to all N cached rows, and everything after
+    attention runs on the active rows only. The hidden state of the active
+    tokens therefore stays compact (one row per active token) from the patch
+    embedding through the last layer to the velocity head.
+  * Section 2.4, Eq. 6 -- the velocity head's output refreshes v_hat[A_i];
+    then every token takes the Euler step with its cached velocity.
+  * Section 2.2 and Appendix B -- group sizes |G_k| are fixed; membership is
+    set by ranking tokens on a per-token velocity statistic, smaller values
+    to lower budgets.
+
+Readings where the paper is silent:
+  * A stack layer is the self-attention sub-layer with its residual,
+    h <- h + Attn_l(h) W_o^T; no norms, modulation, cross-attention or FFN.
+    The residual stream is stored in the model dtype, rounded once per layer
+    (the product and the add are formed exactly, then rounded).
+  * Patch embedding: a linear map of the C values of a patch token (16
+    latent channels times a 1x2x2 patch = 64) to d, no bias; the fp32
+    latent rows are rounded once to the model dtype first. Velocity head: a
+    linear map d -> C with an fp32 output. No timestep conditioning.
+  * Group refresh: at the iterations i with i mod P == 0, P = lcm over the
+    budgets of T/s_k -- the iterations at which every group's schedule fires,
+    so every token has just produced a fresh velocity -- tokens are ranked
+    by the squared L2 norm of their velocity, ascending, and the fixed group
+    sizes are filled in ascending budget order. The key is the float64 sum
+    of the squared fp32 components, added in channel order (each square is
+    exact in float64); keys compare as their IEEE bit patterns (a total
+    order on non-negative values) and ties go to the lower token index. The
+    new budgets hold from iteration i + 1.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from .hsa_oracle import active_set, attention, cached_euler, qkv_cache_update, round_to
+
+
+# ---------------------------------------------------------------------------
+# Compact per-row maps (patch embedding, residual output projection, head)
+# ---------------------------------------------------------------------------
+
+
+def gather_latent(x, idx, dtype: str) -> np.ndarray:
+    """Rows idx of the fp32 latent, rounded once to the model dtype."""
+    return round_to(np.asarray(x, np.float64)[np.asarray(idx, np.int64)], dtype)
+
+
+def linear(a, w, dtype: str, residual=None) -> np.ndarray:
+    """a W^T (+ residual) formed in float64, rounded once to dtype. w is
+    [d_out, d_in]."""
+    acc = np.asarray(a, np.float64) @ np.asarray(w, np.float64).T
+    if residual is not None:
+        acc = acc + np.asarray(residual, np.float64)
+    return round_to(acc, dtype)
+
+
+# ---------------------------------------------------------------------------
+# Group refresh from velocity norms
+# ---------------------------------------------------------------------------
+
+
+def velocity_keys(v) -> np.ndarray:
+    """Per-token squared L2 norm of the fp32 velocity rows: float64, summed
+    over channels in channel order."""
+    v = np.asarray(v, np.float64)
+    acc = np.zeros(v.shape[0], dtype=np.float64)
+    for c in range(v.shape[1]):
+        acc = acc + v[:, c] * v[:, c]
+    return acc
+
+
+def token_ranks(keys) -> np.ndarray:
+    """rank[n] = number of tokens before n in ascending (key, index) order;
+    keys compare by their float64 bit patterns."""
+    k = np.ascontiguousarray(keys, dtype=np.float64).view(np.uint64)
+    order = np.lexsort((np.arange(k.size), k))
+    rank = np.empty(k.size, dtype=np.int64)
+    rank[order] = np.arange(k.size)
+    return rank
+
+
+def check_group_sizes(group_sizes, N: int, T: int | None = None) -> tuple:
+    """((s_k, n_k), ...) in strictly ascending budget order, sizes summing to N."""
+    gs = tuple((int(s), int(n)) for s, n in group_sizes)
+    if not gs:
+        raise ValueError("no groups")
+    if any(b[0] <= a[0] for a, b in zip(gs, gs[1:])):
+        raise ValueError("budgets must be strictly ascending")
+    if any(n < 0 for _, n in gs) or sum(n for _, n in gs) != N:
+        raise ValueError("group sizes must be non-negative and sum to N")
+    if T is not None and any(s < 1 or s > T or T % s for s, _ in gs):
+        raise ValueError("every budget must divide T")
+    return gs
+
+
+def assign_groups(v, group_sizes) -> np.ndarray:
+    """Budgets from the velocity rows: the n_1 lowest-ranked tokens get s_1,
+    the next n_2 get s_2, and so on (int32[N])."""
+    v = np.asarray(v)
+    gs = check_group_sizes(group_sizes, v.shape[0])
+    rank = token_ranks(velocity_keys(v))
+    bounds = np.cumsum([n for _, n in gs])
+    g = np.searchsorted(bounds, rank, side="right")
+    return np.array([s for s, _ in gs], dtype=np.int32)[g]
+
+
+def boundary_gaps(keys, group_sizes) -> np.ndarray:
+    """Relative gap between the last key of each group and the first key of
+    the next one in ranked order (how far a group decision is from a tie)."""
+    k = np.sort(np.asarray(keys, np.float64))
+    gaps = []
+    edge = 0
+    for _, n in list(group_sizes)[:-1]:
+        edge += n
+        if 0 < edge < k.size:
+            gaps.append((k[edge] - k[edge - 1]) / max(k[edge], np.finfo(np.float64).tiny))
+    return np.array(gaps)
+
+
+def refresh_period(T: int, budgets) -> int:
+    """P = lcm of T/s_k: every group's schedule fires at the multiples of P."""
+    p = 1
+    for s in budgets:
+        p = p * (T // int(s)) // math.gcd(p, T // int(s))
+    return p
+
+
+# ---------------------------------------------------------------------------
+# Stack forward on the active rows, one iteration, a trajectory
+# ---------------------------------------------------------------------------
+
+
+def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: str) -> dict:
+    """Embedding, L layers and the velocity head for the active rows.
+
+    xa: [|A|, C] model-dtype latent rows of the tokens idx. caches: one
+    (K_hat, V_hat) pair of [N, d] arrays per layer. Returns the fp32-valued
+    fresh velocities [|A|, C], new copies of the caches (rows outside idx
+    untouched) and the compact hidden state entering each layer and leaving
+    the last one.
+    """
+    scale = 1.0 / math.sqrt(dh)
+    h = linear(xa, weights["w_embed"], dtype)
+    hidden = [h]
+    new_caches = []
+    for lw, (k_hat, v_hat) in zip(weights["layers"], caches):
+        r = qkv_cache_update(h, idx, lw["wq"], lw["wk"], lw["wv"], k_hat, v_hat, dtype, x_compact=True)
+        o = round_to(attention(r["q"], r["k_cache"], r["v_cache"], heads, dh, scale), dtype)
+        h = linear(o, lw["wo"], dtype, residual=h)
+        hidden.append(h)
+        new_caches.append((r["k_cache"], r["v_cache"]))
+    v = linear(h, weights["w_head"], "f32")
+    return {"v_fresh": v, "caches": new_caches, "hidden": hidden}
+
+
+def initial_state(x0, n_layers: int, d: int, T: int) -> dict:
+    """Latent x0 (fp32 values), empty caches and velocity cache, every budget
+    T (iteration 0 activates every token whatever the budgets are)."""
+    x = np.asarray(x0, np.float64)
+    N, C = x.shape
+    return {"x": x, "v_hat": np.zeros((N, C)), "budget": np.full(N, T, dtype=np.int32),
+            "caches": [(np.zeros((N, d)), np.zeros((N, d))) for _ in range(n_layers)]}
+
+
+def stack_iteration(state: dict, weights: dict, i: int, T: int, sigmas, heads: int, dh: int,
+                    dtype: str, group_sizes=None, margin: int = 0) -> dict:
+    """One iteration of the multi-layer HSA sampler.
+
+    A_i from the budgets in force; the stack on the active rows (embedding of
+    the gathered latent, each layer's cache overwrite and attention, the
+    residual output projection, the velocity head); v_hat[A_i] refreshed and
+    every token advanced by Eq. 6; at refresh iterations (group_sizes given
+    and i mod P == 0) the budgets are reassigned from v_hat. Returns the new
+    state plus the active set, the fresh velocities and the hidden states.
+    """
+    x = state["x"]
+    N = x.shape[0]
+    idx = active_set(state["budget"], T, i, margin)
+    xa = gather_latent(x, idx, dtype)
+    f = stack_forward(xa, idx, weights, state["caches"], heads, dh, dtype)
+    x_new, v_hat = cached_euler(x, state["v_hat"], f["v_fresh"], idx, sigmas[i], sigmas[i + 1])
+    budget = state["budget"]
+    refreshed = False
+    if group_sizes is not None:
+        gs = check_group_sizes(group_sizes, N, T)
+        if i % refresh_period(T, [s for s, _ in gs]) == 0:
+            if idx.size != N:
+                raise ValueError("a refresh iteration must have every token active")
+            budget = assign_groups(v_hat, gs)
+            refreshed = True
+    return {"i": i, "idx": idx, "x": x_new, "v_hat": v_hat, "caches": f["caches"], "budget": budget,
+            "refreshed": refreshed, "v_fresh": f["v_fresh"], "hidden": f["hidden"]}
+
+
+def stack_trajectory(x0, weights: dict, T: int, sigmas, heads: int, dh: int, dtype: str,
+                     group_sizes=None, margin: int = 0, iterations=None, state=None) -> list:
+    """Iterations 0..T-1 (or the first `iterations`) of the multi-layer
+    sampler from initial_state (or the given state). With group_sizes None
+    and every budget T this is the dense flow-matching loop. Returns one
+    record per iteration."""
+    d = heads * dh
+    if state is None:
+        state = initial_state(x0, len(weights["layers"]), d, T)
+    records = []
+    for i in range(T if iterations is None else iterations):
+        r = stack_iteration(state, weights, i, T, sigmas, heads, dh, dtype, group_sizes, margin)
+        records.append(r)
+        state = {"x": r["x"], "v_hat": r["v_hat"], "budget": r["budget"], "caches": r["caches"]}
+    return records

@@ -15,6 +15,9 @@ from .workloads import (  # noqa: F401
     draw_block,
     draw_cache,
     draw_euler_state,
+    draw_stack,
+    draw_stack_state,
+    group_sizes,
     linear_sigmas,
     to_bf16_values,
 )

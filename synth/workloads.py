@@ -35,6 +35,8 @@ class Workload:
     C: channels of the Euler state. None means the block output itself is the
     velocity (the Euler state is the block input, C = d).
     iters: iterations at which the workload is measured or checked.
+    layers: self-attention layers of a stack workload (embedding C -> d,
+    `layers` layers, velocity head d -> C); 1 for the single-block workloads.
     """
 
     name: str
@@ -47,6 +49,7 @@ class Workload:
     groups: tuple
     iters: tuple = ()
     C: int | None = None
+    layers: int = 1
     notes: str = field(default="", compare=False)
 
     @property
@@ -82,6 +85,24 @@ WORKLOADS = {
         "wan14b_720p", (21, 45, 80), 5120, 40, 128, "bf16", 40,
         ((40, 0.25), (10, 0.25), (5, 0.5)), iters=(1,), C=16,
         notes="N=75600, d=5120, 40x128, bf16; iteration 1 has 25% active; Euler over N x 16 fp32",
+    ),
+    # Stacks for the multi-layer sampling loop: latent of C = 64 values per
+    # patch token (16 channels x a 1x2x2 patch), embedding C -> d, `layers`
+    # self-attention layers with residual, velocity head d -> C.
+    "tiny_stack_f32": Workload(
+        "tiny_stack_f32", (3, 10, 10), 128, 2, 64, "f32", 8,
+        ((8, 1 / 3), (4, 1 / 3), (2, 1 / 3)), iters=tuple(range(8)), C=16, layers=3,
+        notes="N=300, d=128, 2x64, fp32, C=16, 3 layers; T=8, budgets {8,4,2} in thirds",
+    ),
+    "small_stack_bf16": Workload(
+        "small_stack_bf16", (2, 20, 25), 256, 2, 128, "bf16", 8,
+        ((8, 0.25), (4, 0.25), (2, 0.5)), iters=(0, 1, 2), C=64, layers=4,
+        notes="N=1000, d=256, 2x128, bf16, C=64, 4 layers; T=8, budgets {8:25%, 4:25%, 2:50%}",
+    ),
+    "wan1.3b_stack": Workload(
+        "wan1.3b_stack", (21, 30, 52), 1536, 12, 128, "bf16", 40,
+        ((40, 0.25), (20, 0.25), (10, 0.25), (5, 0.25)), iters=tuple(range(40)), C=64, layers=30,
+        notes="N=32760, d=1536, 12x128, bf16, C=64, 30 layers; T=40, budgets {40,20,10,5} in quarters",
     ),
 }
 
@@ -159,11 +180,7 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
     Appendix B), seeded from the v_group values.
     """
     N = v_group.shape[0]
-    order_groups = sorted(groups, key=lambda g: g[0])  # ascending budget
-    sizes = [int(math.floor(N * f)) for _, f in order_groups[:-1]]
-    sizes.append(N - sum(sizes))
-    if min(sizes) < 0:
-        raise ValueError("group fractions exceed 1")
+    order_groups = group_sizes(N, groups)
     if layout == "scattered":
         norms = np.sqrt(np.sum(v_group.astype(np.float64) ** 2, axis=1))
         rank = np.argsort(norms, kind="stable")
@@ -176,10 +193,58 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
         raise ValueError(f"unknown layout {layout!r}")
     budget = np.empty(N, dtype=np.int32)
     start = 0
-    for (s, _), n in zip(order_groups, sizes):
+    for s, n in order_groups:
         budget[rank[start:start + n]] = s
         start += n
     return budget
+
+
+def group_sizes(N: int, groups) -> tuple:
+    """((s_k, |G_k|), ...) in ascending budget order for N tokens: floor(N *
+    fraction) for every budget except the largest, which takes the rest."""
+    order_groups = sorted(groups, key=lambda g: g[0])
+    sizes = [int(math.floor(N * f)) for _, f in order_groups[:-1]]
+    sizes.append(N - sum(sizes))
+    if min(sizes) < 0:
+        raise ValueError("group fractions exceed 1")
+    return tuple((int(s), n) for (s, _), n in zip(order_groups, sizes))
+
+
+def draw_stack(wl: Workload, seed: int = 0, n_tokens: int | None = None, layers: int | None = None):
+    """Initial latent and random-init weights of a stack workload, drawn in the
+    fixed order x0, W_embed, then Wq, Wk, Wv, Wo of each layer, then W_head.
+
+    x0 ~ N(0, 1) fp32 [N, C] (the latent at sigma = 1); W_embed ~ N(0, 1/C)
+    [d, C]; layer weights ~ N(0, 1/d) [d, d]; W_head ~ N(0, 1/d) [C, d]; all
+    [d_out, d_in]. Weights are bf16-valued for bf16 workloads.
+    """
+    N = wl.N if n_tokens is None else int(n_tokens)
+    L = wl.layers if layers is None else int(layers)
+    d, C = wl.d, wl.euler_channels
+    rng = np.random.default_rng([seed, 0x57AC])
+    cast = to_bf16_values if wl.dtype == "bf16" else (lambda a: a)
+    x0 = _normal(rng, (N, C))
+    w_embed = cast(_normal(rng, (d, C), 1.0 / math.sqrt(C)))
+    layer_ws = []
+    for _ in range(L):
+        ws = [cast(_normal(rng, (d, d), 1.0 / math.sqrt(d))) for _ in range(4)]
+        layer_ws.append(dict(zip(("wq", "wk", "wv", "wo"), ws)))
+    w_head = cast(_normal(rng, (C, d), 1.0 / math.sqrt(d)))
+    return {"x0": x0, "w_embed": w_embed, "layers": layer_ws, "w_head": w_head}
+
+
+def draw_stack_state(wl: Workload, seed: int, n_tokens: int | None = None, layers: int | None = None):
+    """A mid-trajectory state of a stack workload: latent x and velocity cache
+    [N, C] fp32 ~ N(0, 1) and one (K_hat, V_hat) pair [N, d] ~ N(0, 1) per
+    layer (model dtype values), standing in for what earlier iterations left."""
+    N = wl.N if n_tokens is None else int(n_tokens)
+    L = wl.layers if layers is None else int(layers)
+    rng = np.random.default_rng([seed, 0x5747])
+    cast = to_bf16_values if wl.dtype == "bf16" else (lambda a: a)
+    x = _normal(rng, (N, wl.euler_channels))
+    v_hat = _normal(rng, (N, wl.euler_channels))
+    caches = [(cast(_normal(rng, (N, wl.d))), cast(_normal(rng, (N, wl.d)))) for _ in range(L)]
+    return {"x": x, "v_hat": v_hat, "caches": caches}
 
 
 def linear_sigmas(T: int) -> np.ndarray:
