@@ -172,6 +172,135 @@ int hsa_cached_euler(float* x, float* v_cache, const float* v_fresh, const int32
                      int32_t n_active, int64_t n_tokens, int32_t channels, float sigma_i,
                      float sigma_next, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Multi-layer sampling loop.
+ *
+ * A stack of self-attention layers driven by the HSA schedule (Sections
+ * 2.2-2.4): the active tokens' latent rows are embedded, every layer
+ * recomputes Q/K/V for those rows only, overwrites their rows of its own
+ * cache and attends to all N cached rows, and the hidden state of the active
+ * tokens stays compact (one row per active token) from the embedding to the
+ * velocity head. A stack layer is h <- h + Attn(h) Wo^T; the patch
+ * embedding maps the C latent values of a token to d, the velocity head maps
+ * d back to C (fp32). Weights are [d_out, d_in], no biases.
+ * ------------------------------------------------------------------------ */
+
+/*
+ * Active rows of the fp32 latent in the model dtype (the embedding input):
+ *   xa[j][c] = dtype(x[idx[j]][c]) for j < n_active, c < channels,
+ * bf16 rounded to nearest even. Rows whose index lies outside [0, n_tokens)
+ * are written as zeros.
+ *   x    [n_tokens, channels] fp32     xa   [n_active, channels] dtype
+ * xa must not overlap x or idx.
+ */
+int hsa_gather_rows(int dtype, const float* x, const int32_t* idx, int32_t n_active,
+                    int64_t n_tokens, int32_t channels, void* xa, hipStream_t stream);
+
+/*
+ * Compact row map of the stack (the embedding, the residual output
+ * projection of a layer, the velocity head; Section 2.3: after attention
+ * every per-token computation runs on the active rows only):
+ *   y[m] = x[m] W^T (+ residual[m]),  m < n_rows,
+ * accumulated in fp32 and rounded once to out_dtype.
+ *   x         [n_rows, d_in] dtype     w  [d_out, d_in] dtype
+ *   residual  NULL or [n_rows, d_out] out_dtype; it may be y itself (in-place
+ *             h += ...), but must not overlap y otherwise
+ *   y         [n_rows, d_out] out_dtype
+ * out_dtype is dtype, or HSA_STEP_F32 with dtype HSA_STEP_BF16 (then no
+ * residual). bf16 inputs need d_in % 64 == 0, d_out % 4 == 0 and 16-byte
+ * aligned pointers. y must not overlap x or w.
+ */
+int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, const void* w,
+               int32_t d_out, const void* residual, int out_dtype, void* y, hipStream_t stream);
+
+/* Bytes of device workspace hsa_assign_budgets needs: 8 * n_tokens. */
+size_t hsa_assign_budgets_workspace_bytes(int64_t n_tokens);
+
+/*
+ * Group refresh from velocity norms (Section 2.2 and Appendix B: group
+ * sizes are fixed, membership follows a per-token velocity statistic,
+ * smaller values to lower budgets). For every token t:
+ *   key[t]  = sum over c = 0, 1, ..., channels-1 of v[t][c]^2 in float64
+ *             (exact squares, added in channel order);
+ *   rank[t] = number of tokens u with key[u] < key[t], or key[u] == key[t]
+ *             and u < t (keys compared as IEEE bit patterns, NaN keys as one
+ *             canonical positive NaN above every number);
+ *   budget[t] = group_budget[k] for the group k with
+ *               sum_{j<k} group_size[j] <= rank[t] < sum_{j<=k} group_size[j].
+ *   v             [n_tokens, channels] fp32 velocities
+ *   group_budget  HOST array, n_groups budgets, strictly ascending, each a
+ *                 divisor of T (Eq. 5)
+ *   group_size    HOST array, n_groups sizes >= 0 summing to n_tokens
+ *   n_groups      1 .. 16
+ *   budget        [n_tokens] int32, overwritten
+ *   workspace     device buffer of hsa_assign_budgets_workspace_bytes
+ * Group-table errors return HSA_STEP_ERR_BUDGET before any launch.
+ */
+int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channels, int32_t T,
+                       const int32_t* group_budget, const int64_t* group_size, int32_t n_groups,
+                       int32_t* budget, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
+/*
+ * Device state and caller-owned scratch of one stack. Every pointer except
+ * the two host arrays is a device pointer, 16-byte aligned. d = heads *
+ * head_dim, N = n_tokens, C = channels, es = 2 (bf16) or 4 (fp32).
+ */
+typedef struct hsa_stack {
+  int32_t dtype;      /* HSA_STEP_BF16 or HSA_STEP_F32: weights, caches, hidden state */
+  int32_t n_layers;   /* >= 0 */
+  int32_t heads;
+  int32_t head_dim;   /* 64 or 128 */
+  int32_t channels;   /* C; bf16 stacks need C % 64 == 0 */
+  int32_t reserved;   /* 0 */
+  int64_t n_tokens;   /* N >= 1 */
+  const void* w_embed;            /* [d, C] */
+  const void* w_head;             /* [C, d] */
+  const void* const* w_layers;    /* HOST array of 4 * n_layers pointers: Wq, Wk, Wv, Wo of
+                                     layer 0, then of layer 1, ...; each [d, d] */
+  void* const* caches;            /* HOST array of 2 * n_layers pointers: K_hat, V_hat of
+                                     layer 0, then of layer 1, ...; each [N, d] */
+  float* x;                       /* [N, C] latent, advanced in place */
+  float* v_hat;                   /* [N, C] velocity cache */
+  int32_t* budget;                /* [N] step budgets, rewritten at refresh iterations */
+  int32_t* idx;                   /* scratch [N] int32: the active set */
+  int32_t* n_active;              /* scratch [1] int32 */
+  void* xa;                       /* scratch [N, C] dtype */
+  void* h;                        /* scratch [N, d] dtype: compact hidden state */
+  void* q;                        /* scratch [N, d] dtype */
+  void* o;                        /* scratch [N, d] dtype */
+  float* v_fresh;                 /* scratch [N, C] fp32 */
+  void* keys;                     /* scratch 8 * N bytes (used by refresh iterations) */
+} hsa_stack;
+
+/*
+ * One iteration i of the multi-layer HSA sampler (Sections 2.2-2.4):
+ *   1. A_i from the budgets (and the margin of Section 2.5), as
+ *      hsa_build_active_set; |A_i| is copied to the host (one stream
+ *      synchronization per iteration);
+ *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of h, cache rows A_i
+ *      overwritten, attention of the |A_i| queries against all N cached rows
+ *      (scale 1/sqrt(head_dim)), h <- h + O Wo^T; v_fresh = h W_head^T;
+ *   3. v_hat[A_i] = v_fresh, then x <- x + v_hat (sigma_next - sigma_i) for
+ *      all tokens (Eq. 6, as hsa_cached_euler);
+ *   4. if n_groups > 0 and i is a multiple of P = lcm over the group budgets
+ *      of T / s_k (the iterations where every group's schedule fires), the
+ *      budgets are reassigned from v_hat as hsa_assign_budgets; they hold
+ *      from iteration i + 1. A refresh iteration where not every token is
+ *      active returns HSA_STEP_ERR_BUDGET after step 3 (the budgets in force
+ *      did not come from the group table).
+ * Iteration 0 activates every token whatever the budgets are, which fills
+ * every cache and the velocity cache; later iterations read cache rows
+ * written earlier. n_groups == 0 and every budget T is the dense loop.
+ *   n_active_host   if not NULL: |A_i|
+ *   refreshed_host  if not NULL: 1 if the budgets were reassigned, else 0
+ * Writable buffers must not overlap each other or any weight.
+ */
+int hsa_stack_iteration(const hsa_stack* stack, int32_t T, int32_t iter, int32_t margin,
+                        float sigma_i, float sigma_next, const int32_t* group_budget,
+                        const int64_t* group_size, int32_t n_groups, int32_t* n_active_host,
+                        int32_t* refreshed_host, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -88,8 +88,10 @@ def velocity_keys(v) -> np.ndarray:
 def token_ranks(keys) -> np.ndarray:
     """rank[n] = number of tokens before n in ascending (key, index) order;
     keys compare by their float64 bit patterns."""
-    k = np.ascontiguousarray(keys, dtype=np.float64).view(np.uint64)
-    order = np.lexsort((np.arange(k.size), k))
+    k = np.array(keys, dtype=np.float64)
+    k[np.isnan(k)] = np.nan  # one canonical positive NaN, above every number
+    k = k.view(np.uint64)
+    order = np.lexsort((np.arange(k.size), k))  # key first, then token index
     rank = np.empty(k.size, dtype=np.int64)
     rank[order] = np.arange(k.size)
     return rank

@@ -53,7 +53,9 @@ hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int 
 
 // C[crow(m)][n] = sum_k A[arow(m)][k] * B_z[n][k] for up to three (B, C, c_rows)
 // outputs sharing A. a_rows / c_rows may be null (identity); rows whose index is
-// outside [0, a_limit) / [0, c_limit) are skipped.
+// outside [0, a_limit) / [0, c_limit) are skipped. Single-output products may
+// add a residual R indexed like C (R[crow(m)][n], same leading dimension; R may
+// be C itself) before the one rounding, and a bf16 product may store fp32.
 struct RowGemmOut {
   const void* B;
   void* C;
@@ -68,6 +70,8 @@ struct RowGemm {
   long lda, ldb, ldc;
   RowGemmOut out[3];
   int n_out;
+  const void* residual;  // n_out == 1 only; in the output's dtype
+  int c_f32;             // bf16 inputs, fp32 output (no residual)
 };
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s);
 
@@ -91,5 +95,30 @@ hipError_t launch_attention_f32(const void* q, const void* k, const void* v, voi
 hipError_t launch_cached_euler(float* x, float* v_cache, const float* v_fresh,
                                const int32_t* idx, int n_active, long n_tokens, int channels,
                                float dsig, hipStream_t s);
+
+}  // namespace hsa
+
+// Multi-layer sampling loop (stack.hip).
+namespace hsa {
+
+// xa[j][c] = x[idx[j]][c] in the model dtype (bf16 rounded to nearest even,
+// or fp32); rows whose index is outside [0, n_tokens) are written as zeros.
+hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active, long n_tokens,
+                                int channels, bool out_bf16, void* xa, hipStream_t s);
+
+// Budget groups in ascending budget order: group k holds the tokens of rank
+// end[k-1] .. end[k]-1 (end[-1] = 0) and gets step budget budget[k].
+constexpr int kMaxGroups = 16;
+struct GroupTable {
+  int n;
+  int32_t budget[kMaxGroups];
+  int64_t end[kMaxGroups];
+};
+
+// Group refresh: keys[t] = squared L2 norm of v[t] (float64, channel order),
+// then budget[t] from the rank of (keys[t], t).
+hipError_t launch_assign_budgets(const float* v, long n_tokens, int channels,
+                                 const GroupTable& tab, double* keys, int32_t* budget,
+                                 hipStream_t s);
 
 }  // namespace hsa

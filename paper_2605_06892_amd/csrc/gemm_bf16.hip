@@ -43,10 +43,14 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >
 
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
+// Epilogues: bf16 store, bf16 store of (product + bf16 residual) rounded
+// once, fp32 store.
+enum Epilogue { kEpiBf16 = 0, kEpiBf16Residual = 1, kEpiF32 = 2 };
+
 // NOUT (1 or 3) is the number of outputs sharing A; it is a template
 // parameter so the Q/K/V projection and the output projection are distinct
 // kernels in profiles.
-template <int BM, int BN, int WM, int NOUT>
+template <int BM, int BN, int WM, int NOUT, int EPI>
 __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
   constexpr int WN = kWaves / WM;
   constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
@@ -171,7 +175,6 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
 
   // acc[i][j][e]: output row m = tile row + i*32 + l32,
   //               column n = tile col + j*32 + (e/4)*8 + hi*4 + e%4
-  bf16* __restrict__ C = static_cast<bf16*>(oz.C);
   const int32_t* c_rows = oz.c_rows;
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
@@ -179,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
     if (m >= g.M) continue;
     const int crow = c_rows ? c_rows[m] : m;
     if (crow < 0 || crow >= oz.c_limit) continue;
-    bf16* out = C + (long)crow * g.ldc;
+    const long obase = (long)crow * g.ldc;
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
 #pragma unroll
@@ -188,17 +191,26 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
         if (n < g.Nc) {
           f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                      acc[i][j][4 * q + 3]};
-          *reinterpret_cast<bf16x4*>(out + n) = to_bf16x4(v);
+          if constexpr (EPI == kEpiF32) {
+            *reinterpret_cast<f32x4*>(static_cast<float*>(oz.C) + obase + n) = v;
+          } else {
+            if constexpr (EPI == kEpiBf16Residual) {
+              const bf16x4 r =
+                  *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + obase + n);
+              v += __builtin_convertvector(r, f32x4);
+            }
+            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(oz.C) + obase + n) = to_bf16x4(v);
+          }
         }
       }
     }
   }
 }
 
-template <int BM, int BN, int WM, int NOUT>
+template <int BM, int BN, int WM, int NOUT, int EPI>
 hipError_t launch(const RowGemm& g, hipStream_t s) {
   const long tiles = (long)((g.M + BM - 1) / BM) * ((g.Nc + BN - 1) / BN) * NOUT;
-  hipLaunchKernelGGL((row_gemm_bf16_kernel<BM, BN, WM, NOUT>), dim3((unsigned)tiles),
+  hipLaunchKernelGGL((row_gemm_bf16_kernel<BM, BN, WM, NOUT, EPI>), dim3((unsigned)tiles),
                      dim3(kThreads), 0, s, g);
   return hipGetLastError();
 }
@@ -210,8 +222,10 @@ hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   // 256 x 256 tiles (8 waves of 128 x 64) for the three-output projection;
   // 256 x 128 tiles (8 waves of 64 x 64) for the single-output one, whose grid
   // would otherwise leave CUs idle in the last round of workgroups.
-  if (g.n_out == 3) return launch<256, 256, 2, 3>(g, s);
-  return launch<256, 128, 4, 1>(g, s);
+  if (g.n_out == 3) return launch<256, 256, 2, 3, kEpiBf16>(g, s);
+  if (g.c_f32) return launch<256, 128, 4, 1, kEpiF32>(g, s);
+  if (g.residual) return launch<256, 128, 4, 1, kEpiBf16Residual>(g, s);
+  return launch<256, 128, 4, 1, kEpiBf16>(g, s);
 }
 
 }  // namespace hsa

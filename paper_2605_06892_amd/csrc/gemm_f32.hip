@@ -3,7 +3,8 @@
 //
 // Plain FMA tiling: a 64 x 64 output tile per 256-thread workgroup, each
 // thread accumulating a 4 x 4 block, K step 16 staged through LDS. Arbitrary
-// M, Nc and K (ragged edges are masked).
+// M, Nc and K (ragged edges are masked). An optional fp32 residual, indexed
+// like the output, is added before the store.
 #include "common.h"
 
 namespace hsa {
@@ -67,7 +68,8 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
     __syncthreads();
   }
 
-  float* __restrict__ C = static_cast<float*>(oz.C);
+  float* C = static_cast<float*>(oz.C);  // may alias the residual
+  const float* R = static_cast<const float*>(g.residual);
   const int32_t* c_rows = oz.c_rows;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -78,7 +80,10 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = tn * TN + tx * 4 + j;
-      if (n < g.Nc) C[(long)crow * g.ldc + n] = acc[i][j];
+      if (n < g.Nc) {
+        const long e = (long)crow * g.ldc + n;
+        C[e] = R ? acc[i][j] + R[e] : acc[i][j];
+      }
     }
   }
 }

@@ -1,0 +1,192 @@
+// Kernels of the multi-layer sampling loop that are not matrix products.
+//
+//   * gather_latent: the fp32 latent rows of the active tokens, converted to
+//     the model dtype, as the compact input of the patch embedding (Section
+//     2.3: only the active rows flow through the model).
+//   * velocity_keys + rank_budgets: the group refresh. Group sizes are fixed
+//     and membership follows a per-token velocity ranking (Section 2.2,
+//     Appendix B): the key of a token is the squared L2 norm of its velocity,
+//     a float64 sum of the exact squares in channel order, and its rank is
+//     its position in ascending (key, token) order, keys compared as their
+//     IEEE bit patterns (a total order on non-negative doubles; NaN keys are
+//     made the canonical positive NaN, above every number). The n_1 lowest
+//     ranks get budget s_1, the next n_2 get s_2, and so on.
+//
+// All three are small (N x C fp32 reads, N budgets): one pass each, grid-stride
+// loops; the ranking compares every pair of keys from LDS tiles, O(N^2) VALU
+// work that runs once per refresh.
+#include "common.h"
+
+namespace hsa {
+namespace {
+
+constexpr int kThreads = 256;
+
+int grid_for(long work) {
+  long g = (work + kThreads - 1) / kThreads;
+  if (g > 4096) g = 4096;
+  if (g < 1) g = 1;
+  return (int)g;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void gather_latent_vec(const f32x4* __restrict__ x,
+                                                              const int32_t* __restrict__ idx,
+                                                              int n_active, long n_tokens, int vpr,
+                                                              void* __restrict__ xa) {
+  const long total = (long)n_active * vpr;
+  for (long e = blockIdx.x * (long)kThreads + threadIdx.x; e < total;
+       e += (long)gridDim.x * kThreads) {
+    const long j = e / vpr;
+    const int c = (int)(e - j * vpr);
+    const int t = idx[j];
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (t >= 0 && t < n_tokens) v = x[(long)t * vpr + c];
+    if constexpr (BF16)
+      static_cast<bf16x4*>(xa)[e] = to_bf16x4(v);
+    else
+      static_cast<f32x4*>(xa)[e] = v;
+  }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void gather_latent_scalar(const float* __restrict__ x,
+                                                                 const int32_t* __restrict__ idx,
+                                                                 int n_active, long n_tokens,
+                                                                 int channels,
+                                                                 void* __restrict__ xa) {
+  const long total = (long)n_active * channels;
+  for (long e = blockIdx.x * (long)kThreads + threadIdx.x; e < total;
+       e += (long)gridDim.x * kThreads) {
+    const long j = e / channels;
+    const int c = (int)(e - j * channels);
+    const int t = idx[j];
+    const float v = (t >= 0 && t < n_tokens) ? x[(long)t * channels + c] : 0.f;
+    if constexpr (BF16)
+      static_cast<bf16*>(xa)[e] = (bf16)v;
+    else
+      static_cast<float*>(xa)[e] = v;
+  }
+}
+
+__device__ __forceinline__ double canonical_key(double acc) {
+  return acc != acc ? __longlong_as_double(0x7FF8000000000000LL) : acc;
+}
+
+// one thread per token; channel order is the summation order
+__global__ __launch_bounds__(kThreads) void velocity_keys_vec(const f32x4* __restrict__ v, long n,
+                                                              int vpr, double* __restrict__ keys) {
+  for (long t = blockIdx.x * (long)kThreads + threadIdx.x; t < n; t += (long)gridDim.x * kThreads) {
+    const f32x4* row = v + t * vpr;
+    double acc = 0.0;
+    for (int c = 0; c < vpr; ++c) {
+      const f32x4 e = row[c];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const double w = e[u];
+        acc = acc + w * w;  // w * w is exact in float64
+      }
+    }
+    keys[t] = canonical_key(acc);
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void velocity_keys_scalar(const float* __restrict__ v,
+                                                                 long n, int channels,
+                                                                 double* __restrict__ keys) {
+  for (long t = blockIdx.x * (long)kThreads + threadIdx.x; t < n; t += (long)gridDim.x * kThreads) {
+    const float* row = v + t * channels;
+    double acc = 0.0;
+    for (int c = 0; c < channels; ++c) {
+      const double w = row[c];
+      acc = acc + w * w;
+    }
+    keys[t] = canonical_key(acc);
+  }
+}
+
+// 64 tokens per workgroup (one per lane); the four waves split each LDS tile
+// of keys and their counts are summed at the end.
+constexpr int kRankTokens = 64, kRankTile = 1024;
+
+__global__ __launch_bounds__(kThreads) void rank_budgets(const unsigned long long* __restrict__ keys,
+                                                         int n, GroupTable tab,
+                                                         int32_t* __restrict__ budget) {
+  __shared__ unsigned long long tile[kRankTile];
+  __shared__ int partial[kThreads / kWave][kRankTokens];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int t = blockIdx.x * kRankTokens + lane;
+  const unsigned long long kt = t < n ? keys[t] : 0ull;
+  int count = 0;
+  for (int m0 = 0; m0 < n; m0 += kRankTile) {
+    const int cnt = min(kRankTile, n - m0);
+    __syncthreads();  // the previous tile is no longer read
+    for (int e = threadIdx.x; e < cnt; e += kThreads) tile[e] = keys[m0 + e];
+    __syncthreads();
+    const int lo = wave * (kRankTile / 4);
+    const int hi = min(lo + kRankTile / 4, cnt);
+#pragma unroll 8
+    for (int e = lo; e < hi; ++e) {
+      const unsigned long long km = tile[e];
+      count += (km < kt) | ((km == kt) & (m0 + e < t));
+    }
+  }
+  partial[wave][lane] = count;
+  __syncthreads();
+  if (wave == 0 && t < n) {
+    int r = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / kWave; ++w) r += partial[w][lane];
+    int g = 0;
+    while (g + 1 < tab.n && r >= tab.end[g]) ++g;
+    budget[t] = tab.budget[g];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active, long n_tokens,
+                                int channels, bool out_bf16, void* xa, hipStream_t s) {
+  if (n_active <= 0 || channels <= 0) return hipSuccess;
+  const bool vec = channels % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(xa) & (out_bf16 ? 7 : 15)) == 0;
+  if (vec) {
+    const int vpr = channels / 4;
+    const dim3 grid(grid_for((long)n_active * vpr));
+    if (out_bf16)
+      hipLaunchKernelGGL(gather_latent_vec<true>, grid, dim3(kThreads), 0, s,
+                         reinterpret_cast<const f32x4*>(x), idx, n_active, n_tokens, vpr, xa);
+    else
+      hipLaunchKernelGGL(gather_latent_vec<false>, grid, dim3(kThreads), 0, s,
+                         reinterpret_cast<const f32x4*>(x), idx, n_active, n_tokens, vpr, xa);
+  } else {
+    const dim3 grid(grid_for((long)n_active * channels));
+    if (out_bf16)
+      hipLaunchKernelGGL(gather_latent_scalar<true>, grid, dim3(kThreads), 0, s, x, idx, n_active,
+                         n_tokens, channels, xa);
+    else
+      hipLaunchKernelGGL(gather_latent_scalar<false>, grid, dim3(kThreads), 0, s, x, idx,
+                         n_active, n_tokens, channels, xa);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_assign_budgets(const float* v, long n_tokens, int channels,
+                                 const GroupTable& tab, double* keys, int32_t* budget,
+                                 hipStream_t s) {
+  if (n_tokens <= 0) return hipSuccess;
+  if (channels % 4 == 0 && (reinterpret_cast<uintptr_t>(v) & 15) == 0)
+    hipLaunchKernelGGL(velocity_keys_vec, dim3(grid_for(n_tokens)), dim3(kThreads), 0, s,
+                       reinterpret_cast<const f32x4*>(v), n_tokens, channels / 4, keys);
+  else
+    hipLaunchKernelGGL(velocity_keys_scalar, dim3(grid_for(n_tokens)), dim3(kThreads), 0, s, v,
+                       n_tokens, channels, keys);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned blocks = (unsigned)((n_tokens + kRankTokens - 1) / kRankTokens);
+  hipLaunchKernelGGL(rank_budgets, dim3(blocks), dim3(kThreads), 0, s,
+                     reinterpret_cast<const unsigned long long*>(keys), (int)n_tokens, tab, budget);
+  return hipGetLastError();
+}
+
+}  // namespace hsa

@@ -1,0 +1,272 @@
+// C ABI entry points of the multi-layer sampling loop: host-side argument
+// checks, then kernel launches on the caller's stream. The contract of every
+// call is stated with its declaration in include/hsa_step.h.
+#include <math.h>
+
+#include <vector>
+
+#include "api_util.h"
+
+using namespace hsa_api;
+
+namespace {
+
+struct Span {
+  const void* p;
+  size_t n;
+};
+
+bool any_overlap(const std::vector<Span>& a) {
+  for (size_t i = 0; i < a.size(); ++i)
+    for (size_t j = i + 1; j < a.size(); ++j)
+      if (overlaps(a[i].p, a[i].n, a[j].p, a[j].n)) return true;
+  return false;
+}
+
+bool any_overlap(const std::vector<Span>& a, const std::vector<Span>& b) {
+  for (const Span& x : a)
+    for (const Span& y : b)
+      if (overlaps(x.p, x.n, y.p, y.n)) return true;
+  return false;
+}
+
+// Group table checks (strictly ascending divisors of T, sizes summing to N).
+int make_group_table(int32_t T, const int32_t* gb, const int64_t* gs, int32_t n_groups,
+                     int64_t n_tokens, hsa::GroupTable* tab) {
+  if (n_groups < 1 || n_groups > hsa::kMaxGroups || !gb || !gs) return HSA_STEP_ERR_BUDGET;
+  if (T < 1) return HSA_STEP_ERR_BUDGET;
+  int64_t total = 0;
+  for (int k = 0; k < n_groups; ++k) {
+    if (gb[k] < 1 || gb[k] > T || T % gb[k] != 0) return HSA_STEP_ERR_BUDGET;
+    if (k > 0 && gb[k] <= gb[k - 1]) return HSA_STEP_ERR_BUDGET;
+    if (gs[k] < 0 || gs[k] > n_tokens) return HSA_STEP_ERR_BUDGET;
+    total += gs[k];
+    tab->budget[k] = gb[k];
+    tab->end[k] = total;
+  }
+  if (total != n_tokens) return HSA_STEP_ERR_BUDGET;
+  tab->n = n_groups;
+  return HSA_STEP_OK;
+}
+
+int64_t refresh_period(int32_t T, const int32_t* gb, int32_t n_groups) {
+  int64_t p = 1;
+  for (int k = 0; k < n_groups; ++k) {
+    int64_t q = T / gb[k], a = p, b = q;
+    while (b) {
+      const int64_t r = a % b;
+      a = b;
+      b = r;
+    }
+    p = p / a * q;
+  }
+  return p;
+}
+
+RowGemm compact_gemm(const void* x, int n_rows, int d_in, const void* w, int d_out,
+                     const void* residual, bool f32_out, void* y) {
+  RowGemm g{};
+  g.A = x;
+  g.a_rows = nullptr;
+  g.a_limit = n_rows;
+  g.M = n_rows;
+  g.Nc = d_out;
+  g.K = d_in;
+  g.lda = d_in;
+  g.ldb = d_in;
+  g.ldc = d_out;
+  g.out[0] = {w, y, nullptr, n_rows};
+  g.n_out = 1;
+  g.residual = residual;
+  g.c_f32 = f32_out ? 1 : 0;
+  return g;
+}
+
+hipError_t launch_gemm(int dtype, const RowGemm& g, hipStream_t s) {
+  return dtype == HSA_STEP_BF16 ? hsa::launch_row_gemm_bf16(g, s) : hsa::launch_row_gemm_f32(g, s);
+}
+
+}  // namespace
+
+HSA_API int hsa_gather_rows(int dtype, const float* x, const int32_t* idx, int32_t n_active,
+                            int64_t n_tokens, int32_t channels, void* xa, hipStream_t stream) {
+  const size_t es = elem_size(dtype);
+  if (!es) return HSA_STEP_ERR_DTYPE;
+  if (n_active < 0 || n_tokens < 0 || n_tokens > kMaxRows || channels < 0)
+    return HSA_STEP_ERR_SHAPE;
+  if (n_active == 0 || channels == 0) return HSA_STEP_OK;
+  if (!x || !idx || !xa) return HSA_STEP_ERR_NULL;
+  if (!aligned(x, 4) || !aligned(idx, 4) || !aligned(xa, es)) return HSA_STEP_ERR_SHAPE;
+  const size_t xab = (size_t)n_active * channels * es;
+  if (overlaps(xa, xab, x, (size_t)n_tokens * channels * 4) ||
+      overlaps(xa, xab, idx, (size_t)n_active * 4))
+    return HSA_STEP_ERR_ALIAS;
+  return launch_status(hsa::launch_gather_latent(x, idx, n_active, n_tokens, channels,
+                                                 dtype == HSA_STEP_BF16, xa, stream));
+}
+
+HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, const void* w,
+                       int32_t d_out, const void* residual, int out_dtype, void* y,
+                       hipStream_t stream) {
+  const size_t es = elem_size(dtype), oes = elem_size(out_dtype);
+  if (!es || !oes) return HSA_STEP_ERR_DTYPE;
+  if (out_dtype != dtype && !(dtype == HSA_STEP_BF16 && out_dtype == HSA_STEP_F32))
+    return HSA_STEP_ERR_DTYPE;
+  const bool f32_out = dtype == HSA_STEP_BF16 && out_dtype == HSA_STEP_F32;
+  if (n_rows < 0 || d_in <= 0 || d_out <= 0) return HSA_STEP_ERR_SHAPE;
+  if (f32_out && residual) return HSA_STEP_ERR_SHAPE;
+  if (dtype == HSA_STEP_BF16 && (d_in % 64 != 0 || d_out % 4 != 0)) return HSA_STEP_ERR_SHAPE;
+  if (n_rows == 0) return HSA_STEP_OK;
+  if (!x || !w || !y) return HSA_STEP_ERR_NULL;
+  const size_t align = dtype == HSA_STEP_BF16 ? 16 : 4;
+  if (!aligned(x, align) || !aligned(w, align) || !aligned(y, align) ||
+      (residual && !aligned(residual, align)))
+    return HSA_STEP_ERR_SHAPE;
+  const size_t yb = (size_t)n_rows * d_out * oes;
+  if (overlaps(y, yb, x, (size_t)n_rows * d_in * es) || overlaps(y, yb, w, (size_t)d_out * d_in * es))
+    return HSA_STEP_ERR_ALIAS;
+  if (residual && residual != y && overlaps(y, yb, residual, yb)) return HSA_STEP_ERR_ALIAS;
+  return launch_status(
+      launch_gemm(dtype, compact_gemm(x, n_rows, d_in, w, d_out, residual, f32_out, y), stream));
+}
+
+HSA_API size_t hsa_assign_budgets_workspace_bytes(int64_t n_tokens) {
+  return n_tokens > 0 ? (size_t)n_tokens * 8 : 0;
+}
+
+HSA_API int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channels, int32_t T,
+                               const int32_t* group_budget, const int64_t* group_size,
+                               int32_t n_groups, int32_t* budget, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream) {
+  if (n_tokens < 0 || n_tokens > kMaxRows || channels < 0) return HSA_STEP_ERR_SHAPE;
+  hsa::GroupTable tab{};
+  const int st = make_group_table(T, group_budget, group_size, n_groups, n_tokens, &tab);
+  if (st != HSA_STEP_OK) return st;
+  if (n_tokens == 0) return HSA_STEP_OK;
+  if (!v || !budget) return HSA_STEP_ERR_NULL;
+  const size_t need = hsa_assign_budgets_workspace_bytes(n_tokens);
+  if (!workspace || workspace_bytes < need) return HSA_STEP_ERR_WORKSPACE;
+  if (!aligned(v, 4) || !aligned(budget, 4) || !aligned(workspace, 8)) return HSA_STEP_ERR_SHAPE;
+  const size_t vb = (size_t)n_tokens * channels * 4, bb = (size_t)n_tokens * 4;
+  if (overlaps(budget, bb, v, vb) || overlaps(workspace, need, v, vb) ||
+      overlaps(workspace, need, budget, bb))
+    return HSA_STEP_ERR_ALIAS;
+  return launch_status(hsa::launch_assign_budgets(v, n_tokens, channels, tab,
+                                                  static_cast<double*>(workspace), budget, stream));
+}
+
+HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int32_t margin,
+                                float sigma_i, float sigma_next, const int32_t* group_budget,
+                                const int64_t* group_size, int32_t n_groups,
+                                int32_t* n_active_host, int32_t* refreshed_host,
+                                hipStream_t stream) {
+  if (!s) return HSA_STEP_ERR_NULL;
+  const size_t es = elem_size(s->dtype);
+  if (!es) return HSA_STEP_ERR_DTYPE;
+  const int64_t N = s->n_tokens;
+  const int L = s->n_layers, C = s->channels, dh = s->head_dim;
+  if (N < 1 || N > kMaxRows || L < 0 || s->heads <= 0 || (dh != 64 && dh != 128) || C <= 0 ||
+      s->reserved != 0 || (int64_t)s->heads * dh > INT32_MAX / 4)
+    return HSA_STEP_ERR_SHAPE;
+  const int d = s->heads * dh;
+  if (s->dtype == HSA_STEP_BF16 && C % 64 != 0) return HSA_STEP_ERR_SHAPE;
+  if (T < 1 || iter < 0 || iter >= T || margin < 0 || margin > T / 2) return HSA_STEP_ERR_BUDGET;
+  hsa::GroupTable tab{};
+  if (n_groups != 0) {
+    if (n_groups < 0) return HSA_STEP_ERR_BUDGET;
+    const int st = make_group_table(T, group_budget, group_size, n_groups, N, &tab);
+    if (st != HSA_STEP_OK) return st;
+  }
+  if (!s->w_embed || !s->w_head || !s->x || !s->v_hat || !s->budget || !s->idx || !s->n_active ||
+      !s->xa || !s->h || !s->q || !s->o || !s->v_fresh || (n_groups && !s->keys))
+    return HSA_STEP_ERR_NULL;
+  if (L > 0 && (!s->w_layers || !s->caches)) return HSA_STEP_ERR_NULL;
+  for (int i = 0; i < 4 * L; ++i)
+    if (!s->w_layers[i]) return HSA_STEP_ERR_NULL;
+  for (int i = 0; i < 2 * L; ++i)
+    if (!s->caches[i]) return HSA_STEP_ERR_NULL;
+
+  const size_t row_d = (size_t)d * es, row_c = (size_t)C * es;
+  std::vector<Span> written = {
+      {s->x, (size_t)N * C * 4},   {s->v_hat, (size_t)N * C * 4}, {s->budget, (size_t)N * 4},
+      {s->idx, (size_t)N * 4},     {s->n_active, 4},              {s->xa, (size_t)N * row_c},
+      {s->h, (size_t)N * row_d},   {s->q, (size_t)N * row_d},     {s->o, (size_t)N * row_d},
+      {s->v_fresh, (size_t)N * C * 4}};
+  if (n_groups) written.push_back({s->keys, (size_t)N * 8});
+  for (int i = 0; i < 2 * L; ++i) written.push_back({s->caches[i], (size_t)N * row_d});
+  std::vector<Span> weights = {{s->w_embed, (size_t)d * row_c}, {s->w_head, (size_t)C * row_d}};
+  for (int i = 0; i < 4 * L; ++i) weights.push_back({s->w_layers[i], (size_t)d * row_d});
+  for (const Span& b : written)
+    if (!aligned(b.p, 16)) return HSA_STEP_ERR_SHAPE;
+  for (const Span& b : weights)
+    if (!aligned(b.p, 16)) return HSA_STEP_ERR_SHAPE;
+  if (any_overlap(written) || any_overlap(written, weights)) return HSA_STEP_ERR_ALIAS;
+
+  // 1. active set and its size on the host
+  if (hsa::launch_active_set(s->budget, (int)N, T, iter, margin, s->idx, s->n_active, stream) !=
+      hipSuccess)
+    return HSA_STEP_ERR_LAUNCH;
+  int32_t n = 0;
+  if (hipMemcpyAsync(&n, s->n_active, 4, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return HSA_STEP_ERR_LAUNCH;
+  if (n < 0 || n > N) return HSA_STEP_ERR_BUDGET;
+  if (n_active_host) *n_active_host = n;
+  if (refreshed_host) *refreshed_host = 0;
+
+  // 2. the stack on the active rows
+  const int dt = s->dtype;
+  const bool bf = dt == HSA_STEP_BF16;
+  const float scale = 1.0f / sqrtf((float)dh);
+  if (n > 0) {
+    if (hsa::launch_gather_latent(s->x, s->idx, n, N, C, bf, s->xa, stream) != hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+    if (launch_gemm(dt, compact_gemm(s->xa, n, C, s->w_embed, d, nullptr, false, s->h), stream) !=
+        hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+    for (int l = 0; l < L; ++l) {
+      const void* const* w = s->w_layers + 4 * l;
+      void* kc = s->caches[2 * l];
+      void* vc = s->caches[2 * l + 1];
+      RowGemm g{};
+      g.A = s->h;
+      g.a_rows = nullptr;
+      g.a_limit = n;
+      g.M = n;
+      g.Nc = d;
+      g.K = d;
+      g.lda = g.ldb = g.ldc = d;
+      g.out[0] = {w[0], s->q, nullptr, n};
+      g.out[1] = {w[1], kc, s->idx, (int)N};
+      g.out[2] = {w[2], vc, s->idx, (int)N};
+      g.n_out = 3;
+      if (launch_gemm(dt, g, stream) != hipSuccess) return HSA_STEP_ERR_LAUNCH;
+      const hipError_t e =
+          bf ? hsa::launch_attention_bf16(s->q, kc, vc, s->o, n, (int)N, s->heads, dh, scale, stream)
+             : hsa::launch_attention_f32(s->q, kc, vc, s->o, n, (int)N, s->heads, dh, scale, stream);
+      if (e != hipSuccess) return HSA_STEP_ERR_LAUNCH;
+      if (launch_gemm(dt, compact_gemm(s->o, n, d, w[3], d, s->h, false, s->h), stream) !=
+          hipSuccess)
+        return HSA_STEP_ERR_LAUNCH;
+    }
+    if (launch_gemm(dt, compact_gemm(s->h, n, d, s->w_head, C, nullptr, bf, s->v_fresh), stream) !=
+        hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+  }
+
+  // 3. velocity cache refresh of the active rows, Euler step of every token
+  const float dsig = sigma_next - sigma_i;  // fp32 difference
+  if (hsa::launch_cached_euler(s->x, s->v_hat, n > 0 ? s->v_fresh : nullptr, s->idx, n, N, C, dsig,
+                               stream) != hipSuccess)
+    return HSA_STEP_ERR_LAUNCH;
+
+  // 4. group refresh where every group's schedule fires
+  if (n_groups && iter % refresh_period(T, group_budget, n_groups) == 0) {
+    if (n != N) return HSA_STEP_ERR_BUDGET;
+    if (hsa::launch_assign_budgets(s->v_hat, N, C, tab, static_cast<double*>(s->keys), s->budget,
+                                   stream) != hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+    if (refreshed_host) *refreshed_host = 1;
+  }
+  return HSA_STEP_OK;
+}

@@ -58,6 +58,12 @@ def lib() -> ctypes.CDLL:
             "hsa_attention_workspace_bytes": (S, [ctypes.c_int, I32, I32]),
             "hsa_active_attention": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P, S, P]),
             "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
+            "hsa_gather_rows": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P]),
+            "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, ctypes.c_int, P, P]),
+            "hsa_assign_budgets_workspace_bytes": (S, [I64]),
+            "hsa_assign_budgets": (ctypes.c_int, [P, I64, I32, I32, P, P, I32, P, P, S, P]),
+            "hsa_stack_iteration": (ctypes.c_int, [ctypes.POINTER(HsaStack), I32, I32, I32, F, F, P, P, I32,
+                                                   P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -76,7 +82,28 @@ EXPORTED = (
     "hsa_attention_workspace_bytes",
     "hsa_active_attention",
     "hsa_cached_euler",
+    "hsa_gather_rows",
+    "hsa_linear",
+    "hsa_assign_budgets_workspace_bytes",
+    "hsa_assign_budgets",
+    "hsa_stack_iteration",
 )
+
+
+class HsaStack(ctypes.Structure):
+    """struct hsa_stack of include/hsa_step.h."""
+
+    _fields_ = [
+        ("dtype", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("channels", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("n_tokens", ctypes.c_int64),
+        ("w_embed", ctypes.c_void_p), ("w_head", ctypes.c_void_p),
+        ("w_layers", ctypes.POINTER(ctypes.c_void_p)), ("caches", ctypes.POINTER(ctypes.c_void_p)),
+        ("x", ctypes.c_void_p), ("v_hat", ctypes.c_void_p), ("budget", ctypes.c_void_p),
+        ("idx", ctypes.c_void_p), ("n_active", ctypes.c_void_p), ("xa", ctypes.c_void_p),
+        ("h", ctypes.c_void_p), ("q", ctypes.c_void_p), ("o", ctypes.c_void_p),
+        ("v_fresh", ctypes.c_void_p), ("keys", ctypes.c_void_p),
+    ]
 
 
 def _ptr(t):
@@ -179,3 +206,84 @@ def hsa_cached_euler(x, v_cache, v_fresh, idx, n_active: int, sigma_i: float, si
     st = lib().hsa_cached_euler(_ptr(x), _ptr(v_cache), _ptr(v_fresh), _ptr(idx), n_active, n_tokens,
                                 channels, sigma_i, sigma_next, _stream(stream))
     _check("hsa_cached_euler", st)
+
+
+def hsa_gather_rows(x, idx, n_active: int, xa, stream=None) -> None:
+    """xa[:n_active] = x[idx[:n_active]] in xa's dtype (bf16 or fp32)."""
+    _dev(x, idx, xa)
+    if x.dtype != torch.float32:
+        raise TypeError("the latent is fp32")
+    n_tokens, channels = x.shape
+    st = lib().hsa_gather_rows(_dtype(xa), _ptr(x), _ptr(idx), n_active, n_tokens, channels, _ptr(xa),
+                               _stream(stream))
+    _check("hsa_gather_rows", st)
+
+
+def hsa_linear(x, n_rows: int, w, y, residual=None, stream=None) -> None:
+    """y[:n_rows] = x[:n_rows] w^T (+ residual[:n_rows]); y's dtype is the
+    output dtype (x's, or fp32 for bf16 x)."""
+    _dev(x, w, y, residual)
+    dt = _dtype(x, w)
+    d_out, d_in = w.shape
+    st = lib().hsa_linear(dt, _ptr(x), n_rows, d_in, _ptr(w), d_out, _ptr(residual), _dtype(y), _ptr(y),
+                          _stream(stream))
+    _check("hsa_linear", st)
+
+
+def hsa_assign_budgets_workspace_bytes(n_tokens: int) -> int:
+    return int(lib().hsa_assign_budgets_workspace_bytes(n_tokens))
+
+
+def _group_arrays(group_sizes):
+    n = len(group_sizes)
+    gb = (ctypes.c_int32 * max(n, 1))(*[int(s) for s, _ in group_sizes])
+    gs = (ctypes.c_int64 * max(n, 1))(*[int(c) for _, c in group_sizes])
+    return gb, gs, n
+
+
+def hsa_assign_budgets(v, T: int, group_sizes, budget, workspace, stream=None) -> None:
+    """budget = group of each token's velocity-norm rank; group_sizes is
+    ((s_k, n_k), ...) in ascending budget order."""
+    _dev(v, budget, workspace)
+    n_tokens, channels = v.shape
+    gb, gs, n = _group_arrays(group_sizes)
+    nbytes = workspace.numel() * workspace.element_size()
+    st = lib().hsa_assign_budgets(_ptr(v), n_tokens, channels, T, gb, gs, n, _ptr(budget), _ptr(workspace),
+                                  nbytes, _stream(stream))
+    _check("hsa_assign_budgets", st)
+
+
+def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_active, xa, h, q, o, v_fresh,
+               keys, heads: int, head_dim: int) -> HsaStack:
+    """Fill a struct hsa_stack from device tensors. layers: per layer
+    (wq, wk, wv, wo); caches: per layer (k_hat, v_hat). The returned struct
+    keeps its host pointer arrays alive; the tensors must outlive it."""
+    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys]
+    ts += [t for lw in layers for t in lw] + [t for c in caches for t in c]
+    _dev(*ts)
+    n_tokens, channels = x.shape
+    wl = (ctypes.c_void_p * max(1, 4 * len(layers)))(*[t.data_ptr() for lw in layers for t in lw])
+    cl = (ctypes.c_void_p * max(1, 2 * len(caches)))(*[t.data_ptr() for c in caches for t in c])
+    s = HsaStack(dtype=_dtype(w_embed, w_head, xa, h, q, o, *[t for lw in layers for t in lw],
+                              *[t for c in caches for t in c]),
+                 n_layers=len(layers), heads=heads, head_dim=head_dim, channels=channels, reserved=0,
+                 n_tokens=n_tokens, w_embed=w_embed.data_ptr(), w_head=w_head.data_ptr(),
+                 w_layers=ctypes.cast(wl, ctypes.POINTER(ctypes.c_void_p)),
+                 caches=ctypes.cast(cl, ctypes.POINTER(ctypes.c_void_p)),
+                 x=x.data_ptr(), v_hat=v_hat.data_ptr(), budget=budget.data_ptr(), idx=idx.data_ptr(),
+                 n_active=n_active.data_ptr(), xa=xa.data_ptr(), h=h.data_ptr(), q=q.data_ptr(),
+                 o=o.data_ptr(), v_fresh=v_fresh.data_ptr(), keys=keys.data_ptr())
+    s._keep = (wl, cl)
+    return s
+
+
+def hsa_stack_iteration(stack: HsaStack, T: int, iteration: int, margin: int, sigma_i: float,
+                        sigma_next: float, group_sizes=None, stream=None) -> tuple:
+    """One multi-layer HSA iteration; returns (|A_i|, refreshed)."""
+    gb, gs, n = _group_arrays(group_sizes or ())
+    n_act = ctypes.c_int32(-1)
+    ref = ctypes.c_int32(-1)
+    st = lib().hsa_stack_iteration(ctypes.byref(stack), T, iteration, margin, sigma_i, sigma_next, gb, gs, n,
+                                   ctypes.byref(n_act), ctypes.byref(ref), _stream(stream))
+    _check("hsa_stack_iteration", st)
+    return n_act.value, bool(ref.value)

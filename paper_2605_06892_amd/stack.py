@@ -1,0 +1,91 @@
+"""Device buffers and the iteration loop of a multi-layer HSA sampler.
+
+The stack (patch embedding, self-attention layers with residual and
+per-layer caches, velocity head) and one whole iteration of the sampler run
+inside the HIP library (hsa_stack_iteration); this module only allocates the
+device tensors with torch, fills the struct the library reads and calls it
+once per iteration (Sections 2.2-2.4).
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import torch
+
+from . import hsa_step as H
+
+
+@dataclass
+class StackBuffers:
+    """Weights, state and scratch of one stack of L layers over N tokens."""
+
+    x: torch.Tensor          # [N, C] fp32 latent
+    v_hat: torch.Tensor      # [N, C] fp32 velocity cache
+    budget: torch.Tensor     # int32 [N]
+    w_embed: torch.Tensor    # [d, C]
+    w_head: torch.Tensor     # [C, d]
+    layers: list             # per layer (wq, wk, wv, wo), each [d, d]
+    caches: list             # per layer (k_hat, v_hat), each [N, d]
+    idx: torch.Tensor        # int32 [N]
+    n_active: torch.Tensor   # int32 [1]
+    xa: torch.Tensor         # [N, C] model dtype
+    h: torch.Tensor          # [N, d]
+    q: torch.Tensor          # [N, d]
+    o: torch.Tensor          # [N, d]
+    v_fresh: torch.Tensor    # [N, C] fp32
+    keys: torch.Tensor       # float64 [N]
+    heads: int
+    head_dim: int
+    _handle: H.HsaStack | None = field(default=None, repr=False)
+
+    @property
+    def N(self) -> int:
+        return self.x.shape[0]
+
+    @property
+    def C(self) -> int:
+        return self.x.shape[1]
+
+    @property
+    def d(self) -> int:
+        return self.heads * self.head_dim
+
+    @classmethod
+    def allocate(cls, N: int, C: int, n_layers: int, heads: int, head_dim: int, dtype: torch.dtype,
+                 device="cuda") -> "StackBuffers":
+        d = heads * head_dim
+        e = lambda *s, dt=dtype: torch.empty(*s, dtype=dt, device=device)  # noqa: E731
+        f32 = torch.float32
+        return cls(x=e(N, C, dt=f32), v_hat=e(N, C, dt=f32), budget=e(N, dt=torch.int32),
+                   w_embed=e(d, C), w_head=e(C, d),
+                   layers=[tuple(e(d, d) for _ in range(4)) for _ in range(n_layers)],
+                   caches=[(e(N, d), e(N, d)) for _ in range(n_layers)],
+                   idx=e(N, dt=torch.int32), n_active=e(1, dt=torch.int32), xa=e(N, C), h=e(N, d), q=e(N, d),
+                   o=e(N, d), v_fresh=e(N, C, dt=f32), keys=e(N, dt=torch.float64), heads=heads,
+                   head_dim=head_dim)
+
+    def handle(self) -> H.HsaStack:
+        """The struct hsa_stack describing these tensors (built once)."""
+        if self._handle is None:
+            self._handle = H.make_stack(x=self.x, v_hat=self.v_hat, budget=self.budget, w_embed=self.w_embed,
+                                        w_head=self.w_head, layers=self.layers, caches=self.caches, idx=self.idx,
+                                        n_active=self.n_active, xa=self.xa, h=self.h, q=self.q, o=self.o,
+                                        v_fresh=self.v_fresh, keys=self.keys, heads=self.heads,
+                                        head_dim=self.head_dim)
+        return self._handle
+
+
+def iteration(b: StackBuffers, T: int, i: int, sigmas, group_sizes=None, margin: int = 0,
+              stream=None) -> tuple:
+    """Iteration i of the sampler; returns (|A_i|, refreshed)."""
+    return H.hsa_stack_iteration(b.handle(), T, i, margin, float(sigmas[i]), float(sigmas[i + 1]), group_sizes,
+                                 stream)
+
+
+def run(b: StackBuffers, T: int, sigmas, group_sizes=None, margin: int = 0, iterations=None,
+        start: int = 0, stream=None) -> list:
+    """Iterations start .. start+iterations-1 (default: the whole trajectory);
+    returns the (|A_i|, refreshed) of each."""
+    stop = T if iterations is None else start + iterations
+    return [iteration(b, T, i, sigmas, group_sizes, margin, stream) for i in range(start, stop)]

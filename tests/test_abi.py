@@ -144,3 +144,117 @@ def test_euler_errors(lib):
     assert f(A, B, B + 4, D, 10, 100, 16, 1.0, 0.9, None) == ALIAS     # fresh inside the cache
     # nothing to do is success without touching memory
     assert f(None, None, None, None, 0, 0, 16, 1.0, 0.9, None) == OK
+
+
+def test_stack_struct_layout_matches_the_header(tmp_path):
+    """The ctypes mirror of struct hsa_stack has the C compiler's layout."""
+    fields = [f for f, _ in H.HsaStack._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"hsa_step.h\"\nint main(void) {\n"
+                   "  printf(\"%zu\\n\", sizeof(hsa_stack));\n"
+                   + "".join(f"  printf(\"%zu\\n\", offsetof(hsa_stack, {f}));\n" for f in fields)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    r = subprocess.run(["gcc", "-std=c11", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                        "-I", "/opt/rocm/include", str(src), "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
+    assert got[0] == ctypes.sizeof(H.HsaStack)
+    assert got[1:] == [getattr(H.HsaStack, f).offset for f in fields]
+
+
+def test_gather_rows_errors(lib):
+    f = lib.hsa_gather_rows
+    assert f(3, A, B, 10, 100, 16, C, None) == DTYPE
+    assert f(BF16, A, B, -1, 100, 16, C, None) == SHAPE
+    assert f(BF16, A, B, 10, -1, 16, C, None) == SHAPE
+    assert f(BF16, None, B, 10, 100, 16, C, None) == NULL
+    assert f(BF16, A, B, 10, 100, 16, None, None) == NULL
+    assert f(BF16, A, B, 10, 100, 16, A + 64, None) == ALIAS     # xa inside x
+    assert f(BF16, A, B, 10, 100, 16, B, None) == ALIAS          # xa on top of idx
+    assert f(F32, A + 2, B, 10, 100, 16, C, None) == SHAPE       # misaligned latent
+    assert f(BF16, None, None, 0, 100, 16, None, None) == OK     # nothing to gather
+
+
+def test_linear_errors(lib):
+    f = lib.hsa_linear
+    assert f(F32, A, 10, 64, B, 64, None, BF16, C, None) == DTYPE   # fp32 in, bf16 out
+    assert f(9, A, 10, 64, B, 64, None, BF16, C, None) == DTYPE
+    assert f(BF16, A, 10, 100, B, 64, None, BF16, C, None) == SHAPE  # bf16 d_in % 64
+    assert f(BF16, A, 10, 64, B, 62, None, BF16, C, None) == SHAPE   # bf16 d_out % 4
+    assert f(BF16, A, 10, 64, B, 64, D, F32, C, None) == SHAPE       # fp32 output takes no residual
+    assert f(BF16, A, -1, 64, B, 64, None, BF16, C, None) == SHAPE
+    assert f(BF16, None, 10, 64, B, 64, None, BF16, C, None) == NULL
+    assert f(BF16, A, 10, 64, B, 64, None, BF16, A + 64, None) == ALIAS   # y inside x
+    assert f(BF16, A, 10, 64, B, 64, None, BF16, B, None) == ALIAS        # y on top of w
+    assert f(BF16, A, 10, 64, B, 64, C + 16, BF16, C, None) == ALIAS      # residual partly over y
+    assert f(BF16, A, 10, 64, B, 64, None, BF16, C + 8, None) == SHAPE    # misaligned
+    assert f(BF16, None, 0, 64, None, 64, None, BF16, None, None) == OK
+
+
+def test_assign_budgets_errors(lib):
+    f = lib.hsa_assign_budgets
+    gb = lambda *v: (ctypes.c_int32 * len(v))(*v)  # noqa: E731
+    gs = lambda *v: (ctypes.c_int64 * len(v))(*v)  # noqa: E731
+    ws = lib.hsa_assign_budgets_workspace_bytes(100)
+    assert ws == 800 and lib.hsa_assign_budgets_workspace_bytes(-3) == 0
+    assert f(A, 100, 16, 40, gb(40, 10), gs(50, 50), 2, B, C, ws, None) == BUDGET   # not ascending
+    assert f(A, 100, 16, 40, gb(10, 30), gs(50, 50), 2, B, C, ws, None) == BUDGET   # 30 does not divide 40
+    assert f(A, 100, 16, 40, gb(10, 40), gs(50, 49), 2, B, C, ws, None) == BUDGET   # sizes do not sum to N
+    assert f(A, 100, 16, 40, gb(10, 40), gs(-1, 101), 2, B, C, ws, None) == BUDGET
+    assert f(A, 100, 16, 40, gb(10), gs(100), 0, B, C, ws, None) == BUDGET           # no groups
+    assert f(A, 100, 16, 40, None, gs(100), 1, B, C, ws, None) == BUDGET
+    assert f(A, 100, 16, 40, gb(40), gs(100), 1, B, None, ws, None) == WORKSPACE
+    assert f(A, 100, 16, 40, gb(40), gs(100), 1, B, C, ws - 8, None) == WORKSPACE
+    assert f(None, 100, 16, 40, gb(40), gs(100), 1, B, C, ws, None) == NULL
+    assert f(A, 100, 16, 40, gb(40), gs(100), 1, A + 4, C, ws, None) == ALIAS       # budget inside v
+    assert f(A, 100, 16, 40, gb(40), gs(100), 1, B, B + 8, ws, None) == ALIAS       # workspace over budget
+
+
+def _stack(**over):
+    base = 0x7E0000000000
+    step = 1 << 32
+    ptrs = {n: base + k * step for k, n in enumerate(
+        ["w_embed", "w_head", "x", "v_hat", "budget", "idx", "n_active", "xa", "h", "q", "o", "v_fresh", "keys"])}
+    L = over.pop("L", 2)
+    wl = (ctypes.c_void_p * (4 * L))(*[0x7D0000000000 + k * step for k in range(4 * L)])
+    cl = (ctypes.c_void_p * (2 * L))(*[0x7C0000000000 + k * step for k in range(2 * L)])
+    fields = dict(dtype=BF16, n_layers=L, heads=12, head_dim=128, channels=64, reserved=0, n_tokens=1000,
+                  w_layers=ctypes.cast(wl, ctypes.POINTER(ctypes.c_void_p)),
+                  caches=ctypes.cast(cl, ctypes.POINTER(ctypes.c_void_p)), **ptrs)
+    fields.update(over)
+    s = H.HsaStack(**fields)
+    s._keep = (wl, cl)
+    return s, wl, cl
+
+
+def test_stack_iteration_errors(lib):
+    f = lib.hsa_stack_iteration
+    gb = (ctypes.c_int32 * 2)(20, 40)
+    gs = (ctypes.c_int64 * 2)(500, 500)
+    call = lambda s, T=40, i=1, m=0, g=2, b=gb: f(ctypes.byref(s), T, i, m, 1.0, 0.975, b, gs, g,  # noqa: E731
+                                                  None, None, None)
+    assert f(None, 40, 0, 0, 1.0, 0.975, None, None, 0, None, None, None) == NULL
+    assert call(_stack(dtype=4)[0]) == DTYPE
+    assert call(_stack(head_dim=96)[0]) == SHAPE
+    assert call(_stack(channels=16)[0]) == SHAPE           # bf16 stacks need C % 64 == 0
+    assert call(_stack(n_tokens=0)[0]) == SHAPE
+    assert call(_stack(reserved=1)[0]) == SHAPE
+    assert call(_stack(n_layers=-1, L=1)[0]) == SHAPE
+    assert call(_stack()[0], i=40) == BUDGET
+    assert call(_stack()[0], m=21) == BUDGET
+    assert call(_stack()[0], b=(ctypes.c_int32 * 2)(20, 30)) == BUDGET   # 30 does not divide 40
+    assert call(_stack()[0], g=-1) == BUDGET
+    assert call(_stack(h=None)[0]) == NULL
+    assert call(_stack(keys=None)[0]) == NULL                          # refresh needs the key scratch
+    s, wl, _ = _stack()
+    wl[5] = None
+    assert call(s) == NULL                                             # a missing layer weight
+    s, _, cl = _stack()
+    cl[3] = cl[2] + 64
+    assert call(s) == ALIAS                                            # two caches overlap
+    s, wl, cl = _stack()
+    wl[0] = cl[1]
+    assert call(s) == ALIAS                                            # a weight inside a cache
+    assert call(_stack(q=0x7E0000000000 + 8 * (1 << 32) + 32)[0]) == ALIAS  # q inside h
+    assert call(_stack(o=0x7E0000000000 + 3)[0]) == SHAPE              # misaligned

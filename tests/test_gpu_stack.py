@@ -1,0 +1,275 @@
+"""GPU parity of the multi-layer sampling loop against the CPU oracle.
+
+* hsa_gather_rows, hsa_linear and hsa_assign_budgets on their own: the gather
+  and the group assignment bit for bit, the linear maps within the fp32 /
+  bf16 tolerances.
+* The tiny fp32 stack (N=300, d=128, 3 layers, T=8, budgets {8,4,2}) runs its
+  whole trajectory with group refresh at iterations 0 and 4: active sets and
+  refreshed budgets bit for bit, latent, velocity cache and every layer's
+  caches within 1e-4.
+* The small bf16 stack (N=1000, d=256, 4 layers) runs single iterations from
+  a synthetic mid-trajectory state, partial and refreshing.
+* The Wan-1.3B-shaped 30-layer stack (N=32760, d=1536) runs two iterations in
+  the configuration the benchmark times; checked by properties that hold at
+  any size and by the oracle on a sample of layer-0 cache rows.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import DEV, TOL, host, host_bits, i32, rel_inf, to_dev, torch_dtype
+
+pytest.importorskip("paper_2605_06892_amd.hsa_step")
+from paper_2605_06892_amd import hsa_step as H  # noqa: E402
+from paper_2605_06892_amd import stack as S  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------------------
+# Building blocks
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("dtype,N,C,n_act", [("bf16", 1000, 64, 377), ("f32", 300, 16, 300),
+                                             ("f32", 257, 7, 100), ("bf16", 64, 6, 5)])
+def test_gather_rows(dtype, N, C, n_act):
+    rng = np.random.default_rng(N + C)
+    x = (rng.standard_normal((N, C)) * 3).astype(np.float32)
+    idx = np.sort(rng.choice(N, n_act, replace=False)).astype(np.int32)
+    idx_dev = idx.copy()
+    idx_dev[::17] = -1  # out-of-range rows are written as zeros
+    xa = torch.full((N, C), 7.0, dtype=torch_dtype(dtype), device=DEV)
+    H.hsa_gather_rows(to_dev(x, "f32"), i32(idx_dev), n_act, xa)
+    want = oracle.gather_latent(x, idx, dtype)
+    want[::17] = 0.0
+    np.testing.assert_array_equal(host(xa[:n_act]), want)
+    np.testing.assert_array_equal(host(xa[n_act:]), 7.0)  # rows past n_active untouched
+
+
+@pytest.mark.parametrize("dtype,n,d_in,d_out,mode", [
+    ("bf16", 1000, 64, 256, "plain"),      # embedding
+    ("bf16", 777, 1536, 1536, "residual"),  # residual output projection
+    ("bf16", 300, 256, 64, "f32out"),       # velocity head
+    ("bf16", 33, 1536, 64, "f32out"),
+    ("f32", 300, 16, 128, "plain"),
+    ("f32", 301, 128, 128, "residual"),
+    ("f32", 300, 128, 16, "plain"),
+])
+def test_linear(dtype, n, d_in, d_out, mode):
+    rng = np.random.default_rng(n + d_in + d_out)
+    cast = synth.to_bf16_values if dtype == "bf16" else (lambda a: a)
+    x = cast(rng.standard_normal((n, d_in)).astype(np.float32))
+    w = cast((rng.standard_normal((d_out, d_in)) / np.sqrt(d_in)).astype(np.float32))
+    out_dt = "f32" if mode == "f32out" else dtype
+    if mode == "residual":
+        r = cast(rng.standard_normal((n, d_out)).astype(np.float32))
+        y = to_dev(r, dtype)
+        H.hsa_linear(to_dev(x, dtype), n, to_dev(w, dtype), y, residual=y)  # in place
+        want = oracle.linear(x, w, dtype, residual=r)
+    else:
+        y = torch.zeros((n, d_out), dtype=torch_dtype(out_dt), device=DEV)
+        H.hsa_linear(to_dev(x, dtype), n, to_dev(w, dtype), y)
+        want = oracle.linear(x, w, out_dt)
+    assert rel_inf(host(y), want) <= TOL[out_dt] / (10 if mode == "f32out" else 1)
+    if dtype == "bf16" and out_dt == "bf16":
+        # single rounding of an fp32 accumulation: at most one bf16 ulp off
+        got = host(y)
+        assert np.all(np.abs(got - want) <= np.abs(want) * 2.0 ** -7 + 1e-4 * np.abs(want).max())
+
+
+@pytest.mark.parametrize("N,C,case", [(3000, 64, "normal"), (1000, 16, "normal"), (23, 5, "ties"),
+                                      (32760, 64, "normal"), (700, 64, "nan")])
+def test_assign_budgets(N, C, case):
+    rng = np.random.default_rng(N + C)
+    if case == "ties":
+        v = rng.integers(-3, 4, size=(N, C)).astype(np.float32)
+        v[4] = v[9] = v[17]
+        v[11] = 0.0
+        sizes = ((2, 6), (5, 7), (10, 10))
+        T = 10
+    else:
+        v = rng.standard_normal((N, C)).astype(np.float32)
+        if case == "nan":
+            v[[3, 50, 51], 5] = np.nan
+        sizes = synth.group_sizes(N, ((40, .25), (20, .25), (10, .25), (5, .25)))
+        T = 40
+    budget = torch.full((N,), -5, dtype=torch.int32, device=DEV)
+    ws = torch.empty(H.hsa_assign_budgets_workspace_bytes(N), dtype=torch.uint8, device=DEV)
+    H.hsa_assign_budgets(to_dev(v, "f32"), T, sizes, budget, ws)
+    np.testing.assert_array_equal(budget.cpu().numpy(), oracle.assign_groups(v, sizes))
+    # the keys left in the workspace are the oracle's, bit for bit
+    keys = ws.view(torch.float64).cpu().numpy()
+    np.testing.assert_array_equal(keys.view(np.uint64),
+                                  np.where(np.isnan(oracle.velocity_keys(v)), np.nan,
+                                           oracle.velocity_keys(v)).view(np.uint64))
+
+
+def test_assign_budgets_rejects_bad_groups():
+    v = torch.zeros((8, 4), device=DEV)
+    b = torch.zeros(8, dtype=torch.int32, device=DEV)
+    ws = torch.empty(64, dtype=torch.uint8, device=DEV)
+    for sizes in (((4, 4), (2, 4)), ((2, 4), (4, 3)), ((3, 4), (8, 4))):
+        with pytest.raises(H.HsaStepError) as e:
+            H.hsa_assign_budgets(v, 8, sizes, b, ws)
+        assert e.value.name == "HSA_STEP_ERR_BUDGET"
+    with pytest.raises(H.HsaStepError) as e:
+        H.hsa_assign_budgets(v, 8, ((2, 4), (4, 4)), b, ws[:32])
+    assert e.value.name == "HSA_STEP_ERR_WORKSPACE"
+
+
+# ---------------------------------------------------------------------------
+# Whole iterations
+# ---------------------------------------------------------------------------
+
+
+def _upload(wl, wts, N, L, state=None):
+    b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch_dtype(wl.dtype))
+    b.w_embed.copy_(to_dev(wts["w_embed"], wl.dtype))
+    b.w_head.copy_(to_dev(wts["w_head"], wl.dtype))
+    for dst, lw in zip(b.layers, wts["layers"]):
+        for t, k in zip(dst, ("wq", "wk", "wv", "wo")):
+            t.copy_(to_dev(lw[k], wl.dtype))
+    if state is None:
+        b.x.copy_(to_dev(wts["x0"], "f32"))
+        b.v_hat.zero_()
+        b.budget.fill_(wl.T)
+        for k, v in b.caches:
+            k.zero_()
+            v.zero_()
+    else:
+        b.x.copy_(to_dev(state["x"], "f32"))
+        b.v_hat.copy_(to_dev(state["v_hat"], "f32"))
+        b.budget.copy_(i32(state["budget"]))
+        for (k, v), (kh, vh) in zip(b.caches, state["caches"]):
+            k.copy_(to_dev(kh, wl.dtype))
+            v.copy_(to_dev(vh, wl.dtype))
+    return b
+
+
+def test_tiny_f32_stack_trajectory():
+    wl = synth.WORKLOADS["tiny_stack_f32"]
+    wts = synth.draw_stack(wl, seed=0)
+    sizes = synth.group_sizes(wl.N, wl.groups)
+    sig = synth.linear_sigmas(wl.T)
+    recs = oracle.stack_trajectory(wts["x0"], wts, wl.T, sig, wl.heads, wl.dh, "f32", group_sizes=sizes)
+    b = _upload(wl, wts, wl.N, wl.layers)
+    for r in recs:
+        keys = oracle.velocity_keys(r["v_hat"])
+        n, refreshed = S.iteration(b, wl.T, r["i"], sig, sizes)
+        assert (n, refreshed) == (r["idx"].size, r["refreshed"])
+        np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), r["idx"])
+        if refreshed:  # the ranking decisions are far from ties for this seed
+            assert oracle.boundary_gaps(keys, sizes).min() > TOL["f32"]
+        np.testing.assert_array_equal(b.budget.cpu().numpy(), r["budget"])
+        assert rel_inf(host(b.v_fresh[:n]), r["v_fresh"]) <= TOL["f32"], r["i"]
+        assert rel_inf(host(b.v_hat), r["v_hat"]) <= TOL["f32"], r["i"]
+        assert rel_inf(host(b.x), r["x"]) <= TOL["f32"], r["i"]
+        assert rel_inf(host(b.h[:n]), r["hidden"][-1]) <= TOL["f32"], r["i"]
+        for (k, v), (kr, vr) in zip(b.caches, r["caches"]):
+            assert rel_inf(host(k), kr) <= TOL["f32"], r["i"]
+            assert rel_inf(host(v), vr) <= TOL["f32"], r["i"]
+
+
+def _state_for(wl, seed, N, L):
+    st = synth.draw_stack_state(wl, seed, n_tokens=N, layers=L)
+    st["budget"] = synth.assign_budgets(st["v_hat"], wl.groups)
+    return st
+
+
+@pytest.mark.parametrize("iteration", [1, 2, 0])  # 25% active, 50% active, all active + refresh
+def test_small_bf16_stack_iteration(iteration):
+    wl = synth.WORKLOADS["small_stack_bf16"]
+    N, L = wl.N, wl.layers
+    wts = synth.draw_stack(wl, seed=31)
+    st = _state_for(wl, 32, N, L)
+    sizes = synth.group_sizes(N, wl.groups)
+    sig = synth.linear_sigmas(wl.T)
+    state = {"x": st["x"].astype(np.float64), "v_hat": st["v_hat"].astype(np.float64),
+             "budget": st["budget"],
+             "caches": [(k.astype(np.float64), v.astype(np.float64)) for k, v in st["caches"]]}
+    r = oracle.stack_iteration(state, wts, iteration, wl.T, sig, wl.heads, wl.dh, "bf16", sizes)
+    b = _upload(wl, wts, N, L, st)
+    caches_before = [(host_bits(k), host_bits(v)) for k, v in b.caches]
+    n, refreshed = S.iteration(b, wl.T, iteration, sig, sizes)
+    assert (n, refreshed) == (r["idx"].size, r["refreshed"])
+    np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), r["idx"])
+    skipped = np.setdiff1d(np.arange(N), r["idx"])
+    assert rel_inf(host(b.v_fresh[:n]), r["v_fresh"]) <= TOL["bf16"]
+    assert rel_inf(host(b.h[:n]), r["hidden"][-1]) <= TOL["bf16"]
+    # the Euler update moves x by v_hat * dsig: compare the update itself
+    dx = host(b.x) - st["x"].astype(np.float64)
+    assert rel_inf(dx, r["x"] - st["x"]) <= TOL["bf16"]
+    np.testing.assert_array_equal(host_bits(b.v_hat)[skipped], host_bits(to_dev(st["v_hat"], "f32"))[skipped])
+    for (k, v), (kr, vr), (k0, v0) in zip(b.caches, r["caches"], caches_before):
+        assert rel_inf(host(k), kr) <= TOL["bf16"]
+        assert rel_inf(host(v), vr) <= TOL["bf16"]
+        np.testing.assert_array_equal(host_bits(k)[skipped], k0[skipped])  # untouched rows
+        np.testing.assert_array_equal(host_bits(v)[skipped], v0[skipped])
+    got = b.budget.cpu().numpy()
+    if refreshed:
+        # group sizes are exact; a token may only change group across a
+        # boundary it is within the velocity tolerance of
+        assert [int(np.sum(got == s)) for s, _ in sizes] == [c for _, c in sizes]
+        keys = oracle.velocity_keys(r["v_hat"])
+        ks = np.sort(keys)
+        edges = np.cumsum([c for _, c in sizes])[:-1]
+        bkeys = ks[edges]
+        for t in np.flatnonzero(got != r["budget"]):
+            assert np.min(np.abs(keys[t] - bkeys) / bkeys) < 4 * TOL["bf16"]
+        assert np.mean(got != r["budget"]) < 0.02
+    else:
+        np.testing.assert_array_equal(got, st["budget"])
+
+
+def test_wan13b_stack_iterations():
+    """Two iterations of the 30-layer Wan-1.3B-shaped stack at full size: the
+    all-active first iteration (which fills every cache and refreshes the
+    groups) and the 25%-active second one."""
+    wl = synth.WORKLOADS["wan1.3b_stack"]
+    N, L, C, d = wl.N, wl.layers, wl.euler_channels, wl.d
+    wts = synth.draw_stack(wl, seed=0)
+    sizes = synth.group_sizes(N, wl.groups)
+    sig = synth.linear_sigmas(wl.T)
+    b = _upload(wl, wts, N, L)
+
+    n, refreshed = S.iteration(b, wl.T, 0, sig, sizes)
+    assert (n, refreshed) == (N, True)
+    np.testing.assert_array_equal(b.idx.cpu().numpy(), np.arange(N))
+    v0 = b.v_hat.cpu().numpy()
+    assert np.all(np.isfinite(v0))
+    # refreshed budgets are exactly the ranking of the velocity cache
+    budget1 = b.budget.cpu().numpy()
+    np.testing.assert_array_equal(budget1, oracle.assign_groups(v0, sizes))
+    # Euler from x0 with the fresh velocities: one fp32 rounding of x + v dsig
+    dsig = oracle.euler_delta(sig[0], sig[1])
+    want = oracle.round_f32(wts["x0"].astype(np.float64) + v0.astype(np.float64) * dsig)
+    x1 = b.x.cpu().numpy()
+    assert np.max(np.abs(x1 - want) / np.maximum(np.abs(want), 1e-30)) <= 2.0 ** -23
+    # sampled layer-0 cache rows against the oracle
+    rng = np.random.default_rng(5)
+    rows = np.sort(rng.choice(N, 256, replace=False))
+    h0 = oracle.linear(oracle.gather_latent(wts["x0"], rows, "bf16"), wts["w_embed"], "bf16")
+    k0 = oracle.linear(h0, wts["layers"][0]["wk"], "bf16")
+    v0c = oracle.linear(h0, wts["layers"][0]["wv"], "bf16")
+    assert rel_inf(host(b.caches[0][0][rows]), k0) <= TOL["bf16"]
+    assert rel_inf(host(b.caches[0][1][rows]), v0c) <= TOL["bf16"]
+
+    caches_before = [(k.clone(), v.clone()) for k, v in b.caches]
+    vhat_before = b.v_hat.clone()
+    n, refreshed = S.iteration(b, wl.T, 1, sig, sizes)
+    idx = oracle.active_set(budget1, wl.T, 1)
+    assert (n, refreshed) == (idx.size, False) and n == sizes[-1][1]
+    np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), idx)
+    skipped = torch.from_numpy(np.setdiff1d(np.arange(N), idx)).to(DEV)
+    act = torch.from_numpy(idx).to(DEV)
+    for (k, v), (k0_, v0_) in zip(b.caches, caches_before):
+        assert torch.equal(k[skipped], k0_[skipped]) and torch.equal(v[skipped], v0_[skipped])
+        assert not torch.equal(k[act], k0_[act])
+    assert torch.equal(b.v_hat[skipped], vhat_before[skipped])
+    assert torch.equal(b.v_hat[act], b.v_fresh[:n])
+    assert torch.isfinite(b.v_fresh[:n]).all()
+    np.testing.assert_array_equal(b.budget.cpu().numpy(), budget1)
