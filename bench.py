@@ -59,6 +59,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-schedules", action="store_true", help="skip the preset-schedule trajectories")
     p.add_argument("--no-euler-stress", action="store_true", help="skip the Euler bandwidth-stress shape")
+    p.add_argument("--no-end-to-end", action="store_true",
+                   help="skip the 30-layer sampling loops (HSA vs dense, T = 40)")
+    p.add_argument("--end-to-end-only", action="store_true", help="run only the 30-layer sampling loops")
     p.add_argument("--summarize", metavar="DIR", default=None,
                    help="print a text summary of the rocprofv3 csv output under DIR and exit")
     p.add_argument("--write-traffic", metavar="DIR", default=None,
@@ -321,6 +324,78 @@ def euler_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
             "bytes": nbytes, "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def stack_flops(n_active, N, d, C, layers):
+    """Matrix-product FLOPs of one stack pass over n_active rows: embedding,
+    per layer Q/K/V, attention against N cached rows and the output
+    projection, velocity head."""
+    per_layer = gemm_flops(n_active, d) + attention_flops(n_active, N, d)
+    return 2.0 * n_active * C * d * 2 + layers * per_layer
+
+
+def end_to_end(dev, name="wan1.3b_stack"):
+    """Whole T = 40 sampling loops of the 30-layer Wan-1.3B-shaped stack on the
+    same seed and weights: the HSA loop (budgets {40, 20, 10, 5} on quarters of
+    the tokens, groups refreshed from velocity norms where every schedule
+    fires) and the dense loop (every token at every iteration: flow matching
+    with T = 40). Each loop is timed on the host clock between two device
+    synchronizations, so it includes the per-iteration read-back of |A_i|."""
+    import torch
+
+    import synth
+    from paper_2605_06892_amd import stack as S
+
+    wl = synth.WORKLOADS[name]
+    N, C, L, d, T = wl.N, wl.euler_channels, wl.layers, wl.d, wl.T
+    t_draw = time.perf_counter()
+    wts = synth.draw_stack(wl, seed=0)
+    b = S.StackBuffers.allocate(N, C, L, wl.heads, wl.dh, torch.bfloat16, device=dev)
+    b.w_embed.copy_(synth.bf16_tensor(wts["w_embed"]))
+    b.w_head.copy_(synth.bf16_tensor(wts["w_head"]))
+    for dst, lw in zip(b.layers, wts["layers"]):
+        for t, k in zip(dst, ("wq", "wk", "wv", "wo")):
+            t.copy_(synth.bf16_tensor(lw[k]))
+    x0 = torch.from_numpy(wts["x0"]).to(dev)
+    del wts
+    t_draw = time.perf_counter() - t_draw
+    sizes = synth.group_sizes(N, wl.groups)
+    sig = synth.linear_sigmas(T)
+
+    def reset():
+        b.x.copy_(x0)
+        b.v_hat.zero_()
+        b.budget.fill_(T)
+        torch.cuda.synchronize()
+
+    def loop(groups, iterations=T):
+        reset()
+        t0 = time.perf_counter()
+        res = S.run(b, T, sig, groups, iterations=iterations)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3, res
+
+    loop(sizes, 2)  # warm-up: a dense and a partial iteration
+    dense_ms, dres = loop(None)
+    dense_finite = bool(torch.isfinite(b.x).all())
+    hsa_ms, hres = loop(sizes)
+    hsa_finite = bool(torch.isfinite(b.x).all())
+    dense_fl = sum(stack_flops(n, N, d, C, L) for n, _ in dres)
+    hsa_fl = sum(stack_flops(n, N, d, C, L) for n, _ in hres)
+    return {
+        "workload": (f"{name}: {L} layers, N={N} ({'x'.join(map(str, wl.grid))}), d={d} ({wl.heads}x{wl.dh}), "
+                     f"C={C} fp32 latent, bf16 model, T={T}, budgets {{40,20,10,5}} on quarters by velocity-norm "
+                     f"rank, refreshed every {math.lcm(*[T // s for s, _ in sizes])} iterations"),
+        "dense_T40_ms": round(dense_ms, 1),
+        "hsa_ms": round(hsa_ms, 1),
+        "runtime_vs_dense": round(hsa_ms / dense_ms, 4),
+        "token_step_fraction": round(sum(n for n, _ in hres) / (N * T), 4),
+        "refreshes": int(sum(r for _, r in hres)),
+        "final_latents_finite": dense_finite and hsa_finite,
+        "dense_tflops": round(dense_fl / (dense_ms * 1e-3) / 1e12, 1),
+        "hsa_tflops": round(hsa_fl / (hsa_ms * 1e-3) / 1e12, 1),
+        "setup_s": round(t_draw, 1),
+    }
+
+
 def cpu_baseline(wl, blk, budget, it):
     """The oracle's layer step timed on this host: two bounded samples of the
     active rows (projections, attention against the whole N-row cache, output
@@ -378,6 +453,9 @@ def main():
         sys.exit(1)
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.end_to_end_only:
+        print(json.dumps({"end_to_end": end_to_end(dev)}))
+        return
     wl = synth.WORKLOADS[args.workload]
     sigmas = synth.linear_sigmas(wl.T)
     blk, budget, b, eul = setup(wl, args.layout, dev)
@@ -463,10 +541,15 @@ def main():
         }
     if not args.no_euler_stress:
         out["euler_stress"] = euler_stress(dev)
-    if not args.no_schedules:
+    if not args.no_schedules or not args.no_end_to_end:
         del b, eul
         torch.cuda.empty_cache()
+    if not args.no_schedules:
         out["schedules"] = schedule_runtimes(dev)
+        torch.cuda.empty_cache()
+    if not args.no_end_to_end:
+        out["end_to_end"] = end_to_end(dev)
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, blk, budget, args.iteration)
     print(json.dumps(out))

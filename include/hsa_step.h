@@ -180,9 +180,11 @@ int hsa_cached_euler(float* x, float* v_cache, const float* v_fresh, const int32
  * recomputes Q/K/V for those rows only, overwrites their rows of its own
  * cache and attends to all N cached rows, and the hidden state of the active
  * tokens stays compact (one row per active token) from the embedding to the
- * velocity head. A stack layer is h <- h + Attn(h) Wo^T; the patch
- * embedding maps the C latent values of a token to d, the velocity head maps
- * d back to C (fp32). Weights are [d_out, d_in], no biases.
+ * velocity head. A stack layer is h <- h + Attn(rms(h)) Wo^T with
+ * rms(h) = h / sqrt(mean(h^2) + 1e-6) per row feeding Q/K/V; a final rms()
+ * precedes the head. The patch embedding maps the C latent values of a token
+ * to d, the velocity head maps d back to C (fp32). Weights are [d_out, d_in],
+ * no biases.
  * ------------------------------------------------------------------------ */
 
 /*
@@ -197,21 +199,34 @@ int hsa_gather_rows(int dtype, const float* x, const int32_t* idx, int32_t n_act
                     int64_t n_tokens, int32_t channels, void* xa, hipStream_t stream);
 
 /*
+ * Per-row RMS factor of compact rows (the normalization before a layer's
+ * Q/K/V projections and before the velocity head):
+ *   scale[m] = 1 / sqrt(mean over k < d of x[m][k]^2 + eps),  m < n_rows,
+ * squares summed in fp32. x [n_rows, d] dtype; scale [n_rows] fp32, which
+ * must not overlap x. eps >= 0 and finite.
+ */
+int hsa_row_rms_scale(int dtype, const void* x, int32_t n_rows, int32_t d, float eps,
+                      float* scale, hipStream_t stream);
+
+/*
  * Compact row map of the stack (the embedding, the residual output
  * projection of a layer, the velocity head; Section 2.3: after attention
  * every per-token computation runs on the active rows only):
- *   y[m] = x[m] W^T (+ residual[m]),  m < n_rows,
- * accumulated in fp32 and rounded once to out_dtype.
- *   x         [n_rows, d_in] dtype     w  [d_out, d_in] dtype
- *   residual  NULL or [n_rows, d_out] out_dtype; it may be y itself (in-place
- *             h += ...), but must not overlap y otherwise
- *   y         [n_rows, d_out] out_dtype
+ *   y[m] = s[m] (x[m] W^T) (+ residual[m]),  m < n_rows,
+ * with s = row_scale (1 if NULL), accumulated in fp32 and rounded once to
+ * out_dtype. With row_scale from hsa_row_rms_scale(x) this is rms(x) W^T.
+ *   x          [n_rows, d_in] dtype     w  [d_out, d_in] dtype
+ *   row_scale  NULL or [n_rows] fp32
+ *   residual   NULL or [n_rows, d_out] out_dtype; it may be y itself (in-place
+ *              h += ...), but must not overlap y otherwise
+ *   y          [n_rows, d_out] out_dtype
  * out_dtype is dtype, or HSA_STEP_F32 with dtype HSA_STEP_BF16 (then no
  * residual). bf16 inputs need d_in % 64 == 0, d_out % 4 == 0 and 16-byte
- * aligned pointers. y must not overlap x or w.
+ * aligned pointers. y must not overlap x, w or row_scale.
  */
 int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, const void* w,
-               int32_t d_out, const void* residual, int out_dtype, void* y, hipStream_t stream);
+               int32_t d_out, const float* row_scale, const void* residual, int out_dtype,
+               void* y, hipStream_t stream);
 
 /* Bytes of device workspace hsa_assign_budgets needs: 8 * n_tokens. */
 size_t hsa_assign_budgets_workspace_bytes(int64_t n_tokens);
@@ -271,6 +286,7 @@ typedef struct hsa_stack {
   void* o;                        /* scratch [N, d] dtype */
   float* v_fresh;                 /* scratch [N, C] fp32 */
   void* keys;                     /* scratch 8 * N bytes (used by refresh iterations) */
+  float* row_scale;               /* scratch [N] fp32: per-row RMS factors */
 } hsa_stack;
 
 /*
@@ -278,9 +294,10 @@ typedef struct hsa_stack {
  *   1. A_i from the budgets (and the margin of Section 2.5), as
  *      hsa_build_active_set; |A_i| is copied to the host (one stream
  *      synchronization per iteration);
- *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of h, cache rows A_i
- *      overwritten, attention of the |A_i| queries against all N cached rows
- *      (scale 1/sqrt(head_dim)), h <- h + O Wo^T; v_fresh = h W_head^T;
+ *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of rms(h), cache rows
+ *      A_i overwritten, attention of the |A_i| queries against all N cached
+ *      rows (scale 1/sqrt(head_dim)), h <- h + O Wo^T; then
+ *      v_fresh = rms(h) W_head^T;
  *   3. v_hat[A_i] = v_fresh, then x <- x + v_hat (sigma_next - sigma_i) for
  *      all tokens (Eq. 6, as hsa_cached_euler);
  *   4. if n_groups > 0 and i is a multiple of P = lcm over the group budgets

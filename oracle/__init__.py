@@ -30,6 +30,8 @@ from .stack_oracle import (  # noqa: F401
     initial_state,
     linear,
     refresh_period,
+    rms_normalize,
+    RMS_EPS,
     stack_forward,
     stack_iteration,
     stack_trajectory,

@@ -23,10 +23,16 @@ What it follows, by section of the paper:
     to lower budgets.
 
 Readings where the paper is silent:
-  * A stack layer is the self-attention sub-layer with its residual,
-    h <- h + Attn_l(h) W_o^T; no norms, modulation, cross-attention or FFN.
-    The residual stream is stored in the model dtype, rounded once per layer
-    (the product and the add are formed exactly, then rounded).
+  * A stack layer is the pre-norm self-attention sub-layer with its
+    residual, h <- h + Attn_l(rms(h)) W_o^T, where rms(h) = h / sqrt(mean(h^2)
+    + eps) per row (eps = 1e-6, no learned scale) feeds the Q/K/V
+    projections; no modulation, cross-attention or FFN. The residual stream
+    is stored in the model dtype, rounded once per layer (the product and
+    the add are formed exactly, then rounded). The normalized rows are not
+    stored: each projection of rms(h) is formed exactly and rounded once.
+    A final rms() precedes the velocity head. (Without the norms a random
+    stack's residual stream grows from layer to layer and the sampled
+    latent diverges within a few iterations.)
   * Patch embedding: a linear map of the C values of a patch token (16
     latent channels times a 1x2x2 patch = 64) to d, no bias; the fp32
     latent rows are rounded once to the model dtype first. Velocity head: a
@@ -59,6 +65,15 @@ from .hsa_oracle import active_set, attention, cached_euler, qkv_cache_update, r
 def gather_latent(x, idx, dtype: str) -> np.ndarray:
     """Rows idx of the fp32 latent, rounded once to the model dtype."""
     return round_to(np.asarray(x, np.float64)[np.asarray(idx, np.int64)], dtype)
+
+
+RMS_EPS = 1e-6
+
+
+def rms_normalize(h, eps: float = RMS_EPS) -> np.ndarray:
+    """h / sqrt(mean over the row of h^2 + eps), float64, unrounded."""
+    h = np.asarray(h, np.float64)
+    return h / np.sqrt(np.mean(h * h, axis=1, keepdims=True) + eps)
 
 
 def linear(a, w, dtype: str, residual=None) -> np.ndarray:
@@ -149,7 +164,8 @@ def refresh_period(T: int, budgets) -> int:
 
 
 def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: str) -> dict:
-    """Embedding, L layers and the velocity head for the active rows.
+    """Embedding, L pre-norm layers, final norm and velocity head for the
+    active rows.
 
     xa: [|A|, C] model-dtype latent rows of the tokens idx. caches: one
     (K_hat, V_hat) pair of [N, d] arrays per layer. Returns the fp32-valued
@@ -162,12 +178,13 @@ def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: st
     hidden = [h]
     new_caches = []
     for lw, (k_hat, v_hat) in zip(weights["layers"], caches):
-        r = qkv_cache_update(h, idx, lw["wq"], lw["wk"], lw["wv"], k_hat, v_hat, dtype, x_compact=True)
+        r = qkv_cache_update(rms_normalize(h), idx, lw["wq"], lw["wk"], lw["wv"], k_hat, v_hat, dtype,
+                             x_compact=True)
         o = round_to(attention(r["q"], r["k_cache"], r["v_cache"], heads, dh, scale), dtype)
         h = linear(o, lw["wo"], dtype, residual=h)
         hidden.append(h)
         new_caches.append((r["k_cache"], r["v_cache"]))
-    v = linear(h, weights["w_head"], "f32")
+    v = linear(rms_normalize(h), weights["w_head"], "f32")
     return {"v_fresh": v, "caches": new_caches, "hidden": hidden}
 
 

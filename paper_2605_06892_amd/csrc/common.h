@@ -53,9 +53,11 @@ hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int 
 
 // C[crow(m)][n] = sum_k A[arow(m)][k] * B_z[n][k] for up to three (B, C, c_rows)
 // outputs sharing A. a_rows / c_rows may be null (identity); rows whose index is
-// outside [0, a_limit) / [0, c_limit) are skipped. Single-output products may
-// add a residual R indexed like C (R[crow(m)][n], same leading dimension; R may
-// be C itself) before the one rounding, and a bf16 product may store fp32.
+// outside [0, a_limit) / [0, c_limit) are skipped. Row m of the product may be
+// scaled by row_scale[m] (an RMS normalization of A's rows folded into the
+// product). Single-output products may add a residual R indexed like C
+// (R[crow(m)][n], same leading dimension; R may be C itself) before the one
+// rounding, and a bf16 product may store fp32.
 struct RowGemmOut {
   const void* B;
   void* C;
@@ -70,8 +72,9 @@ struct RowGemm {
   long lda, ldb, ldc;
   RowGemmOut out[3];
   int n_out;
-  const void* residual;  // n_out == 1 only; in the output's dtype
-  int c_f32;             // bf16 inputs, fp32 output (no residual)
+  const void* residual;    // n_out == 1 only; in the output's dtype
+  int c_f32;               // bf16 inputs, fp32 output (no residual)
+  const float* row_scale;  // null, or one factor per product row m < M
 };
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s);
 
@@ -105,6 +108,10 @@ namespace hsa {
 // or fp32); rows whose index is outside [0, n_tokens) are written as zeros.
 hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active, long n_tokens,
                                 int channels, bool out_bf16, void* xa, hipStream_t s);
+
+// scale[m] = 1 / sqrt(mean_k x[m][k]^2 + eps) for m < n_rows (fp32 sums).
+hipError_t launch_row_rms_scale(const void* x, bool bf16_in, int n_rows, int d, float eps,
+                                float* scale, hipStream_t s);
 
 // Budget groups in ascending budget order: group k holds the tokens of rank
 // end[k-1] .. end[k]-1 (end[-1] = 0) and gets step budget budget[k].

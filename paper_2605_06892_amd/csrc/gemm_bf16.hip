@@ -43,8 +43,8 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >
 
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
-// Epilogues: bf16 store, bf16 store of (product + bf16 residual) rounded
-// once, fp32 store.
+// Epilogues (after the optional per-row scale): bf16 store, bf16 store of
+// (product + bf16 residual) rounded once, fp32 store.
 enum Epilogue { kEpiBf16 = 0, kEpiBf16Residual = 1, kEpiF32 = 2 };
 
 // NOUT (1 or 3) is the number of outputs sharing A; it is a template
@@ -183,6 +183,7 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
     const int crow = c_rows ? c_rows[m] : m;
     if (crow < 0 || crow >= oz.c_limit) continue;
     const long obase = (long)crow * g.ldc;
+    const float rs = g.row_scale ? g.row_scale[m] : 1.f;
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
 #pragma unroll
@@ -191,6 +192,7 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
         if (n < g.Nc) {
           f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                      acc[i][j][4 * q + 3]};
+          if (g.row_scale) v *= rs;
           if constexpr (EPI == kEpiF32) {
             *reinterpret_cast<f32x4*>(static_cast<float*>(oz.C) + obase + n) = v;
           } else {

@@ -3,8 +3,9 @@
 //
 // Plain FMA tiling: a 64 x 64 output tile per 256-thread workgroup, each
 // thread accumulating a 4 x 4 block, K step 16 staged through LDS. Arbitrary
-// M, Nc and K (ragged edges are masked). An optional fp32 residual, indexed
-// like the output, is added before the store.
+// M, Nc and K (ragged edges are masked). An optional per-row scale multiplies
+// each product row, and an optional fp32 residual, indexed like the output, is
+// added before the store.
 #include "common.h"
 
 namespace hsa {
@@ -77,12 +78,14 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
     if (m >= g.M) continue;
     const int crow = c_rows ? c_rows[m] : m;
     if (crow < 0 || crow >= oz.c_limit) continue;
+    const float rs = g.row_scale ? g.row_scale[m] : 1.f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = tn * TN + tx * 4 + j;
       if (n < g.Nc) {
         const long e = (long)crow * g.ldc + n;
-        C[e] = R ? acc[i][j] + R[e] : acc[i][j];
+        const float v = g.row_scale ? acc[i][j] * rs : acc[i][j];
+        C[e] = R ? v + R[e] : v;
       }
     }
   }

@@ -12,9 +12,14 @@
 //     made the canonical positive NaN, above every number). The n_1 lowest
 //     ranks get budget s_1, the next n_2 get s_2, and so on.
 //
-// All three are small (N x C fp32 reads, N budgets): one pass each, grid-stride
-// loops; the ranking compares every pair of keys from LDS tiles, O(N^2) VALU
-// work that runs once per refresh.
+//   * row_rms_scale: 1 / sqrt(mean(h^2) + eps) of every compact hidden row, the
+//     RMS normalization before each layer's Q/K/V projections and before the
+//     velocity head. A per-row factor commutes with the projection, so the
+//     normalized rows are never written: the GEMM epilogue scales its rows.
+//
+// All of them are small (N x C fp32 reads, N budgets, one read of the hidden
+// state): one pass each, grid-stride loops; the ranking compares every pair of
+// keys from LDS tiles, O(N^2) VALU work that runs once per refresh.
 #include "common.h"
 
 namespace hsa {
@@ -143,7 +148,63 @@ __global__ __launch_bounds__(kThreads) void rank_budgets(const unsigned long lon
   }
 }
 
+// one wave per row, fp32 sum of squares
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void row_rms_scale(const void* __restrict__ x, int n_rows,
+                                                          int d, float eps, bool vec,
+                                                          float* __restrict__ scale) {
+  const int lane = threadIdx.x & 63;
+  const long row = (long)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6);
+  if (row >= n_rows) return;  // the whole wave leaves together
+  float acc = 0.f;
+  if constexpr (BF16) {
+    const bf16* r = static_cast<const bf16*>(x) + row * d;
+    if (vec) {
+      for (int c = lane * 8; c < d; c += kWave * 8) {
+        const bf16x8 v = *reinterpret_cast<const bf16x8*>(r + c);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float f = (float)v[u];
+          acc = fmaf(f, f, acc);
+        }
+      }
+    } else {
+      for (int c = lane; c < d; c += kWave) {
+        const float f = (float)r[c];
+        acc = fmaf(f, f, acc);
+      }
+    }
+  } else {
+    const float* r = static_cast<const float*>(x) + row * d;
+    if (vec) {
+      for (int c = lane * 4; c < d; c += kWave * 4) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(r + c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc = fmaf(v[u], v[u], acc);
+      }
+    } else {
+      for (int c = lane; c < d; c += kWave) acc = fmaf(r[c], r[c], acc);
+    }
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) scale[row] = 1.0f / sqrtf(acc / (float)d + eps);
+}
+
 }  // namespace
+
+hipError_t launch_row_rms_scale(const void* x, bool bf16_in, int n_rows, int d, float eps,
+                                float* scale, hipStream_t s) {
+  if (n_rows <= 0 || d <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n_rows + kThreads / kWave - 1) / (kThreads / kWave));
+  const bool vec = (reinterpret_cast<uintptr_t>(x) & 15) == 0 && d % (bf16_in ? 8 : 4) == 0;
+  if (bf16_in)
+    hipLaunchKernelGGL(row_rms_scale<true>, dim3(blocks), dim3(kThreads), 0, s, x, n_rows, d, eps,
+                       vec, scale);
+  else
+    hipLaunchKernelGGL(row_rms_scale<false>, dim3(blocks), dim3(kThreads), 0, s, x, n_rows, d,
+                       eps, vec, scale);
+  return hipGetLastError();
+}
 
 hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active, long n_tokens,
                                 int channels, bool out_bf16, void* xa, hipStream_t s) {

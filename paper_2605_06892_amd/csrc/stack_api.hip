@@ -63,8 +63,10 @@ int64_t refresh_period(int32_t T, const int32_t* gb, int32_t n_groups) {
   return p;
 }
 
+constexpr float kRmsEps = 1e-6f;
+
 RowGemm compact_gemm(const void* x, int n_rows, int d_in, const void* w, int d_out,
-                     const void* residual, bool f32_out, void* y) {
+                     const float* row_scale, const void* residual, bool f32_out, void* y) {
   RowGemm g{};
   g.A = x;
   g.a_rows = nullptr;
@@ -79,6 +81,7 @@ RowGemm compact_gemm(const void* x, int n_rows, int d_in, const void* w, int d_o
   g.n_out = 1;
   g.residual = residual;
   g.c_f32 = f32_out ? 1 : 0;
+  g.row_scale = row_scale;
   return g;
 }
 
@@ -105,9 +108,22 @@ HSA_API int hsa_gather_rows(int dtype, const float* x, const int32_t* idx, int32
                                                  dtype == HSA_STEP_BF16, xa, stream));
 }
 
+HSA_API int hsa_row_rms_scale(int dtype, const void* x, int32_t n_rows, int32_t d, float eps,
+                              float* scale, hipStream_t stream) {
+  const size_t es = elem_size(dtype);
+  if (!es) return HSA_STEP_ERR_DTYPE;
+  if (n_rows < 0 || d <= 0 || !(eps >= 0.f) || !isfinite(eps)) return HSA_STEP_ERR_SHAPE;
+  if (n_rows == 0) return HSA_STEP_OK;
+  if (!x || !scale) return HSA_STEP_ERR_NULL;
+  if (!aligned(x, es) || !aligned(scale, 4)) return HSA_STEP_ERR_SHAPE;
+  if (overlaps(scale, (size_t)n_rows * 4, x, (size_t)n_rows * d * es)) return HSA_STEP_ERR_ALIAS;
+  return launch_status(
+      hsa::launch_row_rms_scale(x, dtype == HSA_STEP_BF16, n_rows, d, eps, scale, stream));
+}
+
 HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, const void* w,
-                       int32_t d_out, const void* residual, int out_dtype, void* y,
-                       hipStream_t stream) {
+                       int32_t d_out, const float* row_scale, const void* residual,
+                       int out_dtype, void* y, hipStream_t stream) {
   const size_t es = elem_size(dtype), oes = elem_size(out_dtype);
   if (!es || !oes) return HSA_STEP_ERR_DTYPE;
   if (out_dtype != dtype && !(dtype == HSA_STEP_BF16 && out_dtype == HSA_STEP_F32))
@@ -120,14 +136,15 @@ HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, c
   if (!x || !w || !y) return HSA_STEP_ERR_NULL;
   const size_t align = dtype == HSA_STEP_BF16 ? 16 : 4;
   if (!aligned(x, align) || !aligned(w, align) || !aligned(y, align) ||
-      (residual && !aligned(residual, align)))
+      (residual && !aligned(residual, align)) || (row_scale && !aligned(row_scale, 4)))
     return HSA_STEP_ERR_SHAPE;
   const size_t yb = (size_t)n_rows * d_out * oes;
-  if (overlaps(y, yb, x, (size_t)n_rows * d_in * es) || overlaps(y, yb, w, (size_t)d_out * d_in * es))
+  if (overlaps(y, yb, x, (size_t)n_rows * d_in * es) ||
+      overlaps(y, yb, w, (size_t)d_out * d_in * es) || overlaps(y, yb, row_scale, (size_t)n_rows * 4))
     return HSA_STEP_ERR_ALIAS;
   if (residual && residual != y && overlaps(y, yb, residual, yb)) return HSA_STEP_ERR_ALIAS;
-  return launch_status(
-      launch_gemm(dtype, compact_gemm(x, n_rows, d_in, w, d_out, residual, f32_out, y), stream));
+  return launch_status(launch_gemm(
+      dtype, compact_gemm(x, n_rows, d_in, w, d_out, row_scale, residual, f32_out, y), stream));
 }
 
 HSA_API size_t hsa_assign_budgets_workspace_bytes(int64_t n_tokens) {
@@ -178,7 +195,8 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
     if (st != HSA_STEP_OK) return st;
   }
   if (!s->w_embed || !s->w_head || !s->x || !s->v_hat || !s->budget || !s->idx || !s->n_active ||
-      !s->xa || !s->h || !s->q || !s->o || !s->v_fresh || (n_groups && !s->keys))
+      !s->xa || !s->h || !s->q || !s->o || !s->v_fresh || !s->row_scale ||
+      (n_groups && !s->keys))
     return HSA_STEP_ERR_NULL;
   if (L > 0 && (!s->w_layers || !s->caches)) return HSA_STEP_ERR_NULL;
   for (int i = 0; i < 4 * L; ++i)
@@ -191,7 +209,7 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       {s->x, (size_t)N * C * 4},   {s->v_hat, (size_t)N * C * 4}, {s->budget, (size_t)N * 4},
       {s->idx, (size_t)N * 4},     {s->n_active, 4},              {s->xa, (size_t)N * row_c},
       {s->h, (size_t)N * row_d},   {s->q, (size_t)N * row_d},     {s->o, (size_t)N * row_d},
-      {s->v_fresh, (size_t)N * C * 4}};
+      {s->v_fresh, (size_t)N * C * 4}, {s->row_scale, (size_t)N * 4}};
   if (n_groups) written.push_back({s->keys, (size_t)N * 8});
   for (int i = 0; i < 2 * L; ++i) written.push_back({s->caches[i], (size_t)N * row_d});
   std::vector<Span> weights = {{s->w_embed, (size_t)d * row_c}, {s->w_head, (size_t)C * row_d}};
@@ -221,13 +239,15 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   if (n > 0) {
     if (hsa::launch_gather_latent(s->x, s->idx, n, N, C, bf, s->xa, stream) != hipSuccess)
       return HSA_STEP_ERR_LAUNCH;
-    if (launch_gemm(dt, compact_gemm(s->xa, n, C, s->w_embed, d, nullptr, false, s->h), stream) !=
-        hipSuccess)
+    if (launch_gemm(dt, compact_gemm(s->xa, n, C, s->w_embed, d, nullptr, nullptr, false, s->h),
+                    stream) != hipSuccess)
       return HSA_STEP_ERR_LAUNCH;
     for (int l = 0; l < L; ++l) {
       const void* const* w = s->w_layers + 4 * l;
       void* kc = s->caches[2 * l];
       void* vc = s->caches[2 * l + 1];
+      if (hsa::launch_row_rms_scale(s->h, bf, n, d, kRmsEps, s->row_scale, stream) != hipSuccess)
+        return HSA_STEP_ERR_LAUNCH;
       RowGemm g{};
       g.A = s->h;
       g.a_rows = nullptr;
@@ -240,17 +260,20 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       g.out[1] = {w[1], kc, s->idx, (int)N};
       g.out[2] = {w[2], vc, s->idx, (int)N};
       g.n_out = 3;
+      g.row_scale = s->row_scale;
       if (launch_gemm(dt, g, stream) != hipSuccess) return HSA_STEP_ERR_LAUNCH;
       const hipError_t e =
           bf ? hsa::launch_attention_bf16(s->q, kc, vc, s->o, n, (int)N, s->heads, dh, scale, stream)
              : hsa::launch_attention_f32(s->q, kc, vc, s->o, n, (int)N, s->heads, dh, scale, stream);
       if (e != hipSuccess) return HSA_STEP_ERR_LAUNCH;
-      if (launch_gemm(dt, compact_gemm(s->o, n, d, w[3], d, s->h, false, s->h), stream) !=
+      if (launch_gemm(dt, compact_gemm(s->o, n, d, w[3], d, nullptr, s->h, false, s->h), stream) !=
           hipSuccess)
         return HSA_STEP_ERR_LAUNCH;
     }
-    if (launch_gemm(dt, compact_gemm(s->h, n, d, s->w_head, C, nullptr, bf, s->v_fresh), stream) !=
-        hipSuccess)
+    if (hsa::launch_row_rms_scale(s->h, bf, n, d, kRmsEps, s->row_scale, stream) != hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+    if (launch_gemm(dt, compact_gemm(s->h, n, d, s->w_head, C, s->row_scale, nullptr, bf, s->v_fresh),
+                    stream) != hipSuccess)
       return HSA_STEP_ERR_LAUNCH;
   }
 

@@ -59,7 +59,8 @@ def lib() -> ctypes.CDLL:
             "hsa_active_attention": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P, S, P]),
             "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
             "hsa_gather_rows": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P]),
-            "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, ctypes.c_int, P, P]),
+            "hsa_row_rms_scale": (ctypes.c_int, [ctypes.c_int, P, I32, I32, F, P, P]),
+            "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, P, ctypes.c_int, P, P]),
             "hsa_assign_budgets_workspace_bytes": (S, [I64]),
             "hsa_assign_budgets": (ctypes.c_int, [P, I64, I32, I32, P, P, I32, P, P, S, P]),
             "hsa_stack_iteration": (ctypes.c_int, [ctypes.POINTER(HsaStack), I32, I32, I32, F, F, P, P, I32,
@@ -83,6 +84,7 @@ EXPORTED = (
     "hsa_active_attention",
     "hsa_cached_euler",
     "hsa_gather_rows",
+    "hsa_row_rms_scale",
     "hsa_linear",
     "hsa_assign_budgets_workspace_bytes",
     "hsa_assign_budgets",
@@ -102,7 +104,7 @@ class HsaStack(ctypes.Structure):
         ("x", ctypes.c_void_p), ("v_hat", ctypes.c_void_p), ("budget", ctypes.c_void_p),
         ("idx", ctypes.c_void_p), ("n_active", ctypes.c_void_p), ("xa", ctypes.c_void_p),
         ("h", ctypes.c_void_p), ("q", ctypes.c_void_p), ("o", ctypes.c_void_p),
-        ("v_fresh", ctypes.c_void_p), ("keys", ctypes.c_void_p),
+        ("v_fresh", ctypes.c_void_p), ("keys", ctypes.c_void_p), ("row_scale", ctypes.c_void_p),
     ]
 
 
@@ -219,14 +221,26 @@ def hsa_gather_rows(x, idx, n_active: int, xa, stream=None) -> None:
     _check("hsa_gather_rows", st)
 
 
-def hsa_linear(x, n_rows: int, w, y, residual=None, stream=None) -> None:
-    """y[:n_rows] = x[:n_rows] w^T (+ residual[:n_rows]); y's dtype is the
-    output dtype (x's, or fp32 for bf16 x)."""
-    _dev(x, w, y, residual)
+RMS_EPS = 1e-6  # the eps of the stack's RMS normalization
+
+
+def hsa_row_rms_scale(x, n_rows: int, scale, eps: float = RMS_EPS, stream=None) -> None:
+    """scale[:n_rows] = 1 / sqrt(mean(x[m]^2) + eps) per row."""
+    _dev(x, scale)
+    if scale.dtype != torch.float32:
+        raise TypeError("row scales are fp32")
+    st = lib().hsa_row_rms_scale(_dtype(x), _ptr(x), n_rows, x.shape[1], eps, _ptr(scale), _stream(stream))
+    _check("hsa_row_rms_scale", st)
+
+
+def hsa_linear(x, n_rows: int, w, y, residual=None, row_scale=None, stream=None) -> None:
+    """y[:n_rows] = row_scale * (x[:n_rows] w^T) (+ residual[:n_rows]); y's
+    dtype is the output dtype (x's, or fp32 for bf16 x)."""
+    _dev(x, w, y, residual, row_scale)
     dt = _dtype(x, w)
     d_out, d_in = w.shape
-    st = lib().hsa_linear(dt, _ptr(x), n_rows, d_in, _ptr(w), d_out, _ptr(residual), _dtype(y), _ptr(y),
-                          _stream(stream))
+    st = lib().hsa_linear(dt, _ptr(x), n_rows, d_in, _ptr(w), d_out, _ptr(row_scale), _ptr(residual), _dtype(y),
+                          _ptr(y), _stream(stream))
     _check("hsa_linear", st)
 
 
@@ -254,11 +268,11 @@ def hsa_assign_budgets(v, T: int, group_sizes, budget, workspace, stream=None) -
 
 
 def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_active, xa, h, q, o, v_fresh,
-               keys, heads: int, head_dim: int) -> HsaStack:
+               keys, row_scale, heads: int, head_dim: int) -> HsaStack:
     """Fill a struct hsa_stack from device tensors. layers: per layer
     (wq, wk, wv, wo); caches: per layer (k_hat, v_hat). The returned struct
     keeps its host pointer arrays alive; the tensors must outlive it."""
-    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys]
+    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale]
     ts += [t for lw in layers for t in lw] + [t for c in caches for t in c]
     _dev(*ts)
     n_tokens, channels = x.shape
@@ -272,7 +286,8 @@ def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_acti
                  caches=ctypes.cast(cl, ctypes.POINTER(ctypes.c_void_p)),
                  x=x.data_ptr(), v_hat=v_hat.data_ptr(), budget=budget.data_ptr(), idx=idx.data_ptr(),
                  n_active=n_active.data_ptr(), xa=xa.data_ptr(), h=h.data_ptr(), q=q.data_ptr(),
-                 o=o.data_ptr(), v_fresh=v_fresh.data_ptr(), keys=keys.data_ptr())
+                 o=o.data_ptr(), v_fresh=v_fresh.data_ptr(), keys=keys.data_ptr(),
+                 row_scale=row_scale.data_ptr())
     s._keep = (wl, cl)
     return s
 

@@ -1,10 +1,10 @@
 """Device buffers and the iteration loop of a multi-layer HSA sampler.
 
-The stack (patch embedding, self-attention layers with residual and
-per-layer caches, velocity head) and one whole iteration of the sampler run
-inside the HIP library (hsa_stack_iteration); this module only allocates the
-device tensors with torch, fills the struct the library reads and calls it
-once per iteration (Sections 2.2-2.4).
+The stack (patch embedding, pre-norm self-attention layers with residual and
+per-layer caches, final norm and velocity head) and one whole iteration of
+the sampler run inside the HIP library (hsa_stack_iteration); this module only
+allocates the device tensors with torch, fills the struct the library reads
+and calls it once per iteration (Sections 2.2-2.4).
 """
 
 from __future__ import annotations
@@ -35,6 +35,7 @@ class StackBuffers:
     o: torch.Tensor          # [N, d]
     v_fresh: torch.Tensor    # [N, C] fp32
     keys: torch.Tensor       # float64 [N]
+    row_scale: torch.Tensor  # fp32 [N]
     heads: int
     head_dim: int
     _handle: H.HsaStack | None = field(default=None, repr=False)
@@ -62,8 +63,8 @@ class StackBuffers:
                    layers=[tuple(e(d, d) for _ in range(4)) for _ in range(n_layers)],
                    caches=[(e(N, d), e(N, d)) for _ in range(n_layers)],
                    idx=e(N, dt=torch.int32), n_active=e(1, dt=torch.int32), xa=e(N, C), h=e(N, d), q=e(N, d),
-                   o=e(N, d), v_fresh=e(N, C, dt=f32), keys=e(N, dt=torch.float64), heads=heads,
-                   head_dim=head_dim)
+                   o=e(N, d), v_fresh=e(N, C, dt=f32), keys=e(N, dt=torch.float64), row_scale=e(N, dt=f32),
+                   heads=heads, head_dim=head_dim)
 
     def handle(self) -> H.HsaStack:
         """The struct hsa_stack describing these tensors (built once)."""
@@ -71,8 +72,8 @@ class StackBuffers:
             self._handle = H.make_stack(x=self.x, v_hat=self.v_hat, budget=self.budget, w_embed=self.w_embed,
                                         w_head=self.w_head, layers=self.layers, caches=self.caches, idx=self.idx,
                                         n_active=self.n_active, xa=self.xa, h=self.h, q=self.q, o=self.o,
-                                        v_fresh=self.v_fresh, keys=self.keys, heads=self.heads,
-                                        head_dim=self.head_dim)
+                                        v_fresh=self.v_fresh, keys=self.keys, row_scale=self.row_scale,
+                                        heads=self.heads, head_dim=self.head_dim)
         return self._handle
 
 

@@ -177,7 +177,7 @@ def test_gather_rows_errors(lib):
 
 
 def test_linear_errors(lib):
-    f = lib.hsa_linear
+    f = lambda *a: lib.hsa_linear(*a[:6], a[6] if len(a) > 10 else None, *a[-4:])  # noqa: E731
     assert f(F32, A, 10, 64, B, 64, None, BF16, C, None) == DTYPE   # fp32 in, bf16 out
     assert f(9, A, 10, 64, B, 64, None, BF16, C, None) == DTYPE
     assert f(BF16, A, 10, 100, B, 64, None, BF16, C, None) == SHAPE  # bf16 d_in % 64
@@ -190,6 +190,23 @@ def test_linear_errors(lib):
     assert f(BF16, A, 10, 64, B, 64, C + 16, BF16, C, None) == ALIAS      # residual partly over y
     assert f(BF16, A, 10, 64, B, 64, None, BF16, C + 8, None) == SHAPE    # misaligned
     assert f(BF16, None, 0, 64, None, 64, None, BF16, None, None) == OK
+    g = lib.hsa_linear
+    assert g(BF16, A, 10, 64, B, 64, C + 8, None, BF16, C, None) == ALIAS  # row scales inside y
+    assert g(BF16, A, 10, 64, B, 64, D + 2, None, BF16, C, None) == SHAPE  # misaligned row scales
+
+
+def test_row_rms_scale_errors(lib):
+    f = lib.hsa_row_rms_scale
+    assert f(7, A, 10, 64, 1e-6, B, None) == DTYPE
+    assert f(BF16, A, -1, 64, 1e-6, B, None) == SHAPE
+    assert f(BF16, A, 10, 0, 1e-6, B, None) == SHAPE
+    assert f(BF16, A, 10, 64, -1.0, B, None) == SHAPE
+    assert f(BF16, A, 10, 64, float("inf"), B, None) == SHAPE
+    assert f(BF16, None, 10, 64, 1e-6, B, None) == NULL
+    assert f(BF16, A, 10, 64, 1e-6, None, None) == NULL
+    assert f(BF16, A, 10, 64, 1e-6, A + 64, None) == ALIAS
+    assert f(BF16, A + 1, 10, 64, 1e-6, B, None) == SHAPE
+    assert f(BF16, None, 0, 64, 1e-6, None, None) == OK
 
 
 def test_assign_budgets_errors(lib):
@@ -215,7 +232,8 @@ def _stack(**over):
     base = 0x7E0000000000
     step = 1 << 32
     ptrs = {n: base + k * step for k, n in enumerate(
-        ["w_embed", "w_head", "x", "v_hat", "budget", "idx", "n_active", "xa", "h", "q", "o", "v_fresh", "keys"])}
+        ["w_embed", "w_head", "x", "v_hat", "budget", "idx", "n_active", "xa", "h", "q", "o", "v_fresh", "keys",
+         "row_scale"])}
     L = over.pop("L", 2)
     wl = (ctypes.c_void_p * (4 * L))(*[0x7D0000000000 + k * step for k in range(4 * L)])
     cl = (ctypes.c_void_p * (2 * L))(*[0x7C0000000000 + k * step for k in range(2 * L)])
@@ -247,6 +265,7 @@ def test_stack_iteration_errors(lib):
     assert call(_stack()[0], g=-1) == BUDGET
     assert call(_stack(h=None)[0]) == NULL
     assert call(_stack(keys=None)[0]) == NULL                          # refresh needs the key scratch
+    assert call(_stack(row_scale=None)[0]) == NULL
     s, wl, _ = _stack()
     wl[5] = None
     assert call(s) == NULL                                             # a missing layer weight

@@ -50,31 +50,55 @@ def test_gather_rows(dtype, N, C, n_act):
     np.testing.assert_array_equal(host(xa[n_act:]), 7.0)  # rows past n_active untouched
 
 
+@pytest.mark.parametrize("dtype,n,d", [("bf16", 1000, 256), ("bf16", 777, 1536), ("bf16", 5, 200),
+                                       ("f32", 300, 128), ("f32", 33, 18)])
+def test_row_rms_scale(dtype, n, d):
+    rng = np.random.default_rng(n + d)
+    cast = synth.to_bf16_values if dtype == "bf16" else (lambda a: a)
+    x = cast((rng.standard_normal((n, d)) * rng.uniform(0.01, 30, size=(n, 1))).astype(np.float32))
+    x[0] = 0.0  # an all-zero row: 1 / sqrt(eps)
+    s = torch.zeros(n + 3, device=DEV)
+    H.hsa_row_rms_scale(to_dev(x, dtype), n, s)
+    want = 1.0 / np.sqrt(np.mean(x.astype(np.float64) ** 2, axis=1) + oracle.RMS_EPS)
+    np.testing.assert_allclose(host(s[:n]), want, rtol=2e-6)
+    assert np.all(host(s[n:]) == 0.0)
+
+
 @pytest.mark.parametrize("dtype,n,d_in,d_out,mode", [
     ("bf16", 1000, 64, 256, "plain"),      # embedding
     ("bf16", 777, 1536, 1536, "residual"),  # residual output projection
     ("bf16", 300, 256, 64, "f32out"),       # velocity head
     ("bf16", 33, 1536, 64, "f32out"),
+    ("bf16", 700, 256, 768, "normed"),      # Q/K/V projection of rms(h)
+    ("bf16", 300, 1536, 64, "normed_f32out"),  # head of rms(h)
     ("f32", 300, 16, 128, "plain"),
     ("f32", 301, 128, 128, "residual"),
     ("f32", 300, 128, 16, "plain"),
+    ("f32", 300, 128, 48, "normed"),
 ])
 def test_linear(dtype, n, d_in, d_out, mode):
     rng = np.random.default_rng(n + d_in + d_out)
     cast = synth.to_bf16_values if dtype == "bf16" else (lambda a: a)
-    x = cast(rng.standard_normal((n, d_in)).astype(np.float32))
+    x = cast((rng.standard_normal((n, d_in)) * rng.uniform(0.1, 10, size=(n, 1))).astype(np.float32))
     w = cast((rng.standard_normal((d_out, d_in)) / np.sqrt(d_in)).astype(np.float32))
-    out_dt = "f32" if mode == "f32out" else dtype
+    out_dt = "f32" if mode.endswith("f32out") else dtype
     if mode == "residual":
         r = cast(rng.standard_normal((n, d_out)).astype(np.float32))
         y = to_dev(r, dtype)
         H.hsa_linear(to_dev(x, dtype), n, to_dev(w, dtype), y, residual=y)  # in place
         want = oracle.linear(x, w, dtype, residual=r)
+    elif mode.startswith("normed"):
+        xd = to_dev(x, dtype)
+        s = torch.empty(n, device=DEV)
+        H.hsa_row_rms_scale(xd, n, s)
+        y = torch.zeros((n, d_out), dtype=torch_dtype(out_dt), device=DEV)
+        H.hsa_linear(xd, n, to_dev(w, dtype), y, row_scale=s)
+        want = oracle.linear(oracle.rms_normalize(x), w, out_dt)
     else:
         y = torch.zeros((n, d_out), dtype=torch_dtype(out_dt), device=DEV)
         H.hsa_linear(to_dev(x, dtype), n, to_dev(w, dtype), y)
         want = oracle.linear(x, w, out_dt)
-    assert rel_inf(host(y), want) <= TOL[out_dt] / (10 if mode == "f32out" else 1)
+    assert rel_inf(host(y), want) <= TOL[out_dt] / (10 if out_dt == "f32" and dtype == "bf16" else 1)
     if dtype == "bf16" and out_dt == "bf16":
         # single rounding of an fp32 accumulation: at most one bf16 ulp off
         got = host(y)
@@ -252,7 +276,7 @@ def test_wan13b_stack_iterations():
     # sampled layer-0 cache rows against the oracle
     rng = np.random.default_rng(5)
     rows = np.sort(rng.choice(N, 256, replace=False))
-    h0 = oracle.linear(oracle.gather_latent(wts["x0"], rows, "bf16"), wts["w_embed"], "bf16")
+    h0 = oracle.rms_normalize(oracle.linear(oracle.gather_latent(wts["x0"], rows, "bf16"), wts["w_embed"], "bf16"))
     k0 = oracle.linear(h0, wts["layers"][0]["wk"], "bf16")
     v0c = oracle.linear(h0, wts["layers"][0]["wv"], "bf16")
     assert rel_inf(host(b.caches[0][0][rows]), k0) <= TOL["bf16"]
