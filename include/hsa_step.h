@@ -95,6 +95,23 @@ int hsa_build_active_set(const int32_t* budget, int64_t n_tokens, int32_t T, int
                          int32_t* n_active_host, hipStream_t stream);
 
 /*
+ * The same with a choice of what happens outside the window (Section 2.5
+ * says every token is active there; read literally, the HSA-25 preset of
+ * Appendix C then takes 34.8% of the token-steps instead of its printed 25%).
+ * Outside the window (margin > 0 and i < m or i > T - m - 1) every token is
+ * active iff iter % outside_period == 0, and none is otherwise:
+ *   outside_period 1          the literal rule (= hsa_build_active_set);
+ *   outside_period T / s_max  every token follows the largest budget's
+ *                             schedule there (24.8% for HSA-25).
+ * outside_period must divide T (else HSA_STEP_ERR_BUDGET). Other arguments
+ * as for hsa_build_active_set.
+ */
+int hsa_build_active_set_window(const int32_t* budget, int64_t n_tokens, int32_t T, int32_t iter,
+                                int32_t margin, int32_t outside_period, int32_t* idx,
+                                int32_t* n_active_dev, int32_t* n_active_host,
+                                hipStream_t stream);
+
+/*
  * Fresh Q/K/V for the active rows and the KV-cache overwrite (Section 2.3,
  * steps 1 and 2). For j < n_active, with token t = idx[j]:
  *   input row  r_j = x[t]  (x_compact == 0, x is [n_tokens, d])
@@ -291,9 +308,9 @@ typedef struct hsa_stack {
 
 /*
  * One iteration i of the multi-layer HSA sampler (Sections 2.2-2.4):
- *   1. A_i from the budgets (and the margin of Section 2.5), as
- *      hsa_build_active_set; |A_i| is copied to the host (one stream
- *      synchronization per iteration);
+ *   1. A_i from the budgets (and the margin and outside period of Section
+ *      2.5), as hsa_build_active_set_window; |A_i| is copied to the host (one
+ *      stream synchronization per iteration);
  *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of rms(h), cache rows
  *      A_i overwritten, attention of the |A_i| queries against all N cached
  *      rows (scale 1/sqrt(head_dim)), h <- h + O Wo^T; then
@@ -314,9 +331,9 @@ typedef struct hsa_stack {
  * Writable buffers must not overlap each other or any weight.
  */
 int hsa_stack_iteration(const hsa_stack* stack, int32_t T, int32_t iter, int32_t margin,
-                        float sigma_i, float sigma_next, const int32_t* group_budget,
-                        const int64_t* group_size, int32_t n_groups, int32_t* n_active_host,
-                        int32_t* refreshed_host, hipStream_t stream);
+                        int32_t outside_period, float sigma_i, float sigma_next,
+                        const int32_t* group_budget, const int64_t* group_size, int32_t n_groups,
+                        int32_t* n_active_host, int32_t* refreshed_host, hipStream_t stream);
 
 #ifdef __cplusplus
 }

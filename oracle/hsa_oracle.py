@@ -93,19 +93,27 @@ def check_budgets(budget, T: int) -> np.ndarray:
     return b
 
 
-def active_set(budget, T: int, i: int, margin: int = 0) -> np.ndarray:
+def active_set(budget, T: int, i: int, margin: int = 0, outside_period: int = 1) -> np.ndarray:
     """A_i: ascending indices n with i mod (T / s_n) == 0 (Section 2.2).
 
-    With a phase-aware margin m > 0 (Section 2.5) every token is active for
-    i < m and for i > T - m - 1.
+    With a phase-aware margin m > 0 (Section 2.5) the iterations i < m and
+    i > T - m - 1 lie outside the caching window. The paper's rule activates
+    every token there (outside_period 1). The other reading, under which the
+    HSA-25 preset of Appendix C meets its printed runtime, has every token
+    follow the largest budget's schedule outside the window: all tokens are
+    active iff i mod outside_period == 0, with outside_period = T / s_max.
     """
     b = check_budgets(budget, T)
     if not 0 <= i < T:
         raise ValueError("iteration out of range")
     if not 0 <= margin <= T // 2:
         raise ValueError("margin out of range")
+    if outside_period < 1 or T % outside_period:
+        raise ValueError("outside_period must divide T")
     if margin > 0 and (i < margin or i > T - margin - 1):
-        return np.arange(b.size, dtype=np.int64)
+        if i % outside_period == 0:
+            return np.arange(b.size, dtype=np.int64)
+        return np.zeros(0, dtype=np.int64)
     period = T // b
     return np.flatnonzero(i % period == 0).astype(np.int64)
 

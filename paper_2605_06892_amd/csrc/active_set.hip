@@ -3,7 +3,12 @@
 //
 // Rule (Section 2.2): token n with budget s_n (a divisor of T, Eq. 5) is active
 // at iteration i iff i mod (T / s_n) == 0. Phase-aware window (Section 2.5):
-// with margin m > 0, every token is active for i < m and for i > T - m - 1.
+// with margin m > 0 the iterations i < m and i > T - m - 1 are outside the
+// window, where every token is active -- at every such iteration (the
+// paper's wording, outside period 1), or only where i mod p == 0 for an
+// outside period p (p = T / s_max: every token follows the largest budget's
+// schedule there, the reading under which the HSA-25 preset of Appendix C
+// meets its printed runtime).
 //
 // The budget array is small (4 bytes per token: 131 KB at N = 32760), so one
 // workgroup of 1024 threads walks it in chunks of 16384 tokens: each thread
@@ -23,13 +28,15 @@ constexpr int kChunk = kThreads * kPer;
 constexpr int kMaxTableT = 1024;
 
 // 0: invalid budget, 1: valid and skipped, 2: valid and active.
-__device__ __forceinline__ int classify(int s, int T, int iter, bool all_active) {
+__device__ __forceinline__ int classify(int s, int T, int iter, bool outside, bool outside_active) {
   if (s < 1 || s > T || (T % s) != 0) return 0;
-  return (all_active || (iter % (T / s)) == 0) ? 2 : 1;
+  if (outside) return outside_active ? 2 : 1;
+  return (iter % (T / s)) == 0 ? 2 : 1;
 }
 
 __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __restrict__ budget,
                                                               int n, int T, int iter, int margin,
+                                                              int outside_period,
                                                               int32_t* __restrict__ idx,
                                                               int32_t* __restrict__ n_active) {
   __shared__ int wave_total[kThreads / kWave];
@@ -39,11 +46,13 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
   const int w = t / kWave;
-  const bool all_active = margin > 0 && (iter < margin || iter > T - margin - 1);
+  const bool outside = margin > 0 && (iter < margin || iter > T - margin - 1);
+  const bool outside_active = outside && (iter % outside_period) == 0;
   const bool use_table = T <= kMaxTableT;
   if (t == 0) bad_any = 0;
   if (use_table) {
-    for (int s = t; s <= T; s += kThreads) table[s] = (unsigned char)classify(s, T, iter, all_active);
+    for (int s = t; s <= T; s += kThreads)
+      table[s] = (unsigned char)classify(s, T, iter, outside, outside_active);
   }
   __syncthreads();
 
@@ -74,7 +83,7 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
         const int s = b[r];
         int cls;
         if (use_table) cls = (s >= 1 && s <= T) ? table[s] : 0;
-        else cls = classify(s, T, iter, all_active);
+        else cls = classify(s, T, iter, outside, outside_active);
         bad |= (cls == 0);
         mask |= (cls == 2 ? 1u : 0u) << r;
       }
@@ -112,9 +121,9 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
 }  // namespace
 
 hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int margin,
-                             int32_t* idx, int32_t* n_active, hipStream_t s) {
+                             int outside_period, int32_t* idx, int32_t* n_active, hipStream_t s) {
   hipLaunchKernelGGL(active_set_kernel, dim3(1), dim3(kThreads), 0, s, budget, n, T, iter, margin,
-                     idx, n_active);
+                     outside_period, idx, n_active);
   return hipGetLastError();
 }
 

@@ -49,7 +49,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 namespace hsa {
 
 hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int margin,
-                             int32_t* idx, int32_t* n_active, hipStream_t s);
+                             int outside_period, int32_t* idx, int32_t* n_active, hipStream_t s);
 
 // C[crow(m)][n] = sum_k A[arow(m)][k] * B_z[n][k] for up to three (B, C, c_rows)
 // outputs sharing A. a_rows / c_rows may be null (identity); rows whose index is

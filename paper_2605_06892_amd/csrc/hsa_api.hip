@@ -21,18 +21,20 @@ HSA_API const char* hsa_step_status_string(int status) {
   }
 }
 
-HSA_API int hsa_build_active_set(const int32_t* budget, int64_t n_tokens, int32_t T, int32_t iter,
-                                 int32_t margin, int32_t* idx, int32_t* n_active_dev,
-                                 int32_t* n_active_host, hipStream_t stream) {
+HSA_API int hsa_build_active_set_window(const int32_t* budget, int64_t n_tokens, int32_t T,
+                                        int32_t iter, int32_t margin, int32_t outside_period,
+                                        int32_t* idx, int32_t* n_active_dev,
+                                        int32_t* n_active_host, hipStream_t stream) {
   if (n_tokens < 0 || n_tokens > kMaxRows) return HSA_STEP_ERR_SHAPE;
   if (T < 1 || iter < 0 || iter >= T || margin < 0 || margin > T / 2) return HSA_STEP_ERR_BUDGET;
+  if (outside_period < 1 || T % outside_period != 0) return HSA_STEP_ERR_BUDGET;
   if (!n_active_dev || (n_tokens > 0 && (!budget || !idx))) return HSA_STEP_ERR_NULL;
   const size_t nb = (size_t)n_tokens * 4;
   if (overlaps(idx, nb, budget, nb) || overlaps(n_active_dev, 4, budget, nb) ||
       overlaps(n_active_dev, 4, idx, nb))
     return HSA_STEP_ERR_ALIAS;
-  hipError_t e = hsa::launch_active_set(budget, (int)n_tokens, T, iter, margin, idx, n_active_dev,
-                                        stream);
+  hipError_t e = hsa::launch_active_set(budget, (int)n_tokens, T, iter, margin, outside_period, idx,
+                                        n_active_dev, stream);
   if (e != hipSuccess) return HSA_STEP_ERR_LAUNCH;
   if (n_active_host) {
     int32_t v = 0;
@@ -43,6 +45,13 @@ HSA_API int hsa_build_active_set(const int32_t* budget, int64_t n_tokens, int32_
     if (v < 0) return HSA_STEP_ERR_BUDGET;
   }
   return HSA_STEP_OK;
+}
+
+HSA_API int hsa_build_active_set(const int32_t* budget, int64_t n_tokens, int32_t T, int32_t iter,
+                                 int32_t margin, int32_t* idx, int32_t* n_active_dev,
+                                 int32_t* n_active_host, hipStream_t stream) {
+  return hsa_build_active_set_window(budget, n_tokens, T, iter, margin, 1, idx, n_active_dev,
+                                     n_active_host, stream);
 }
 
 HSA_API int hsa_qkv_scatter(int dtype, const void* x, int32_t x_compact, const int32_t* idx,

@@ -173,7 +173,8 @@ HSA_API int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channel
 }
 
 HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int32_t margin,
-                                float sigma_i, float sigma_next, const int32_t* group_budget,
+                                int32_t outside_period, float sigma_i, float sigma_next,
+                                const int32_t* group_budget,
                                 const int64_t* group_size, int32_t n_groups,
                                 int32_t* n_active_host, int32_t* refreshed_host,
                                 hipStream_t stream) {
@@ -188,6 +189,7 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   const int d = s->heads * dh;
   if (s->dtype == HSA_STEP_BF16 && C % 64 != 0) return HSA_STEP_ERR_SHAPE;
   if (T < 1 || iter < 0 || iter >= T || margin < 0 || margin > T / 2) return HSA_STEP_ERR_BUDGET;
+  if (outside_period < 1 || T % outside_period != 0) return HSA_STEP_ERR_BUDGET;
   hsa::GroupTable tab{};
   if (n_groups != 0) {
     if (n_groups < 0) return HSA_STEP_ERR_BUDGET;
@@ -221,8 +223,8 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   if (any_overlap(written) || any_overlap(written, weights)) return HSA_STEP_ERR_ALIAS;
 
   // 1. active set and its size on the host
-  if (hsa::launch_active_set(s->budget, (int)N, T, iter, margin, s->idx, s->n_active, stream) !=
-      hipSuccess)
+  if (hsa::launch_active_set(s->budget, (int)N, T, iter, margin, outside_period, s->idx,
+                             s->n_active, stream) != hipSuccess)
     return HSA_STEP_ERR_LAUNCH;
   int32_t n = 0;
   if (hipMemcpyAsync(&n, s->n_active, 4, hipMemcpyDeviceToHost, stream) != hipSuccess ||

@@ -52,6 +52,7 @@ def lib() -> ctypes.CDLL:
         sig = {
             "hsa_step_status_string": (ctypes.c_char_p, [ctypes.c_int]),
             "hsa_build_active_set": (ctypes.c_int, [P, I64, I32, I32, I32, P, P, P, P]),
+            "hsa_build_active_set_window": (ctypes.c_int, [P, I64, I32, I32, I32, I32, P, P, P, P]),
             "hsa_qkv_scatter": (ctypes.c_int, [ctypes.c_int, P, I32, P, I32, I64, I32, P, P, P, P, P, P, P]),
             "hsa_attention_core": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P]),
             "hsa_out_scatter": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P, P]),
@@ -63,8 +64,8 @@ def lib() -> ctypes.CDLL:
             "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, P, ctypes.c_int, P, P]),
             "hsa_assign_budgets_workspace_bytes": (S, [I64]),
             "hsa_assign_budgets": (ctypes.c_int, [P, I64, I32, I32, P, P, I32, P, P, S, P]),
-            "hsa_stack_iteration": (ctypes.c_int, [ctypes.POINTER(HsaStack), I32, I32, I32, F, F, P, P, I32,
-                                                   P, P, P]),
+            "hsa_stack_iteration": (ctypes.c_int, [ctypes.POINTER(HsaStack), I32, I32, I32, I32, F, F, P, P,
+                                                   I32, P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -77,6 +78,7 @@ def lib() -> ctypes.CDLL:
 EXPORTED = (
     "hsa_step_status_string",
     "hsa_build_active_set",
+    "hsa_build_active_set_window",
     "hsa_qkv_scatter",
     "hsa_attention_core",
     "hsa_out_scatter",
@@ -142,15 +144,22 @@ def _dev(*ts) -> None:
 
 
 def hsa_build_active_set(budget, T: int, iteration: int, margin: int, idx, n_active_dev,
-                         read_back: bool = True, stream=None):
+                         read_back: bool = True, stream=None, outside_period: int = 1):
     """Fill idx[:|A_i|] with the active set; returns |A_i| when read_back
-    (one stream synchronization), else None."""
+    (one stream synchronization), else None. outside_period != 1 calls
+    hsa_build_active_set_window."""
     _dev(budget, idx, n_active_dev)
     host = ctypes.c_int32(-2)
-    st = lib().hsa_build_active_set(_ptr(budget), budget.numel(), T, iteration, margin, _ptr(idx),
-                                    _ptr(n_active_dev), ctypes.byref(host) if read_back else None,
-                                    _stream(stream))
-    _check("hsa_build_active_set", st)
+    hb = ctypes.byref(host) if read_back else None
+    if outside_period == 1:
+        fn = "hsa_build_active_set"
+        st = lib().hsa_build_active_set(_ptr(budget), budget.numel(), T, iteration, margin, _ptr(idx),
+                                        _ptr(n_active_dev), hb, _stream(stream))
+    else:
+        fn = "hsa_build_active_set_window"
+        st = lib().hsa_build_active_set_window(_ptr(budget), budget.numel(), T, iteration, margin, outside_period,
+                                               _ptr(idx), _ptr(n_active_dev), hb, _stream(stream))
+    _check(fn, st)
     return host.value if read_back else None
 
 
@@ -293,12 +302,12 @@ def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_acti
 
 
 def hsa_stack_iteration(stack: HsaStack, T: int, iteration: int, margin: int, sigma_i: float,
-                        sigma_next: float, group_sizes=None, stream=None) -> tuple:
+                        sigma_next: float, group_sizes=None, stream=None, outside_period: int = 1) -> tuple:
     """One multi-layer HSA iteration; returns (|A_i|, refreshed)."""
     gb, gs, n = _group_arrays(group_sizes or ())
     n_act = ctypes.c_int32(-1)
     ref = ctypes.c_int32(-1)
-    st = lib().hsa_stack_iteration(ctypes.byref(stack), T, iteration, margin, sigma_i, sigma_next, gb, gs, n,
-                                   ctypes.byref(n_act), ctypes.byref(ref), _stream(stream))
+    st = lib().hsa_stack_iteration(ctypes.byref(stack), T, iteration, margin, outside_period, sigma_i, sigma_next,
+                                   gb, gs, n, ctypes.byref(n_act), ctypes.byref(ref), _stream(stream))
     _check("hsa_stack_iteration", st)
     return n_act.value, bool(ref.value)

@@ -72,9 +72,10 @@ def window_margin(center_percent: int, T: int) -> int:
     return ((100 - center_percent) * T) // 200
 
 
-def active_set(b: BlockBuffers, T: int, iteration: int, margin: int = 0) -> int:
+def active_set(b: BlockBuffers, T: int, iteration: int, margin: int = 0, outside_period: int = 1) -> int:
     """A_i into b.idx; returns |A_i| (one stream synchronization)."""
-    return H.hsa_build_active_set(b.budget, T, iteration, margin, b.idx, b.n_active)
+    return H.hsa_build_active_set(b.budget, T, iteration, margin, b.idx, b.n_active,
+                                  outside_period=outside_period)
 
 
 def qkv(b: BlockBuffers, n_active: int, x_compact: bool = False) -> None:

@@ -78,15 +78,15 @@ class StackBuffers:
 
 
 def iteration(b: StackBuffers, T: int, i: int, sigmas, group_sizes=None, margin: int = 0,
-              stream=None) -> tuple:
+              outside_period: int = 1, stream=None) -> tuple:
     """Iteration i of the sampler; returns (|A_i|, refreshed)."""
     return H.hsa_stack_iteration(b.handle(), T, i, margin, float(sigmas[i]), float(sigmas[i + 1]), group_sizes,
-                                 stream)
+                                 stream, outside_period)
 
 
 def run(b: StackBuffers, T: int, sigmas, group_sizes=None, margin: int = 0, iterations=None,
-        start: int = 0, stream=None) -> list:
+        start: int = 0, outside_period: int = 1, stream=None) -> list:
     """Iterations start .. start+iterations-1 (default: the whole trajectory);
     returns the (|A_i|, refreshed) of each."""
     stop = T if iterations is None else start + iterations
-    return [iteration(b, T, i, sigmas, group_sizes, margin, stream) for i in range(start, stop)]
+    return [iteration(b, T, i, sigmas, group_sizes, margin, outside_period, stream) for i in range(start, stop)]

@@ -89,6 +89,10 @@ def test_build_active_set_errors(lib):
     assert f(A, 100, 40, 0, 0, B, None, None, None) == NULL
     assert f(A, 100, 40, 0, 0, A + 8, C, None, None) == ALIAS    # idx overlaps budget
     assert f(A, 100, 40, 0, 0, B, B + 396, None, None) == ALIAS  # count inside idx
+    g = lib.hsa_build_active_set_window
+    assert g(A, 100, 40, 0, 4, 3, B, C, None, None) == BUDGET    # outside period does not divide T
+    assert g(A, 100, 40, 0, 4, 0, B, C, None, None) == BUDGET
+    assert g(A, 100, 40, 0, 4, 2, A + 8, C, None, None) == ALIAS
 
 
 def test_qkv_scatter_errors(lib):
@@ -250,9 +254,9 @@ def test_stack_iteration_errors(lib):
     f = lib.hsa_stack_iteration
     gb = (ctypes.c_int32 * 2)(20, 40)
     gs = (ctypes.c_int64 * 2)(500, 500)
-    call = lambda s, T=40, i=1, m=0, g=2, b=gb: f(ctypes.byref(s), T, i, m, 1.0, 0.975, b, gs, g,  # noqa: E731
-                                                  None, None, None)
-    assert f(None, 40, 0, 0, 1.0, 0.975, None, None, 0, None, None, None) == NULL
+    call = lambda s, T=40, i=1, m=0, g=2, b=gb, p=1: f(ctypes.byref(s), T, i, m, p, 1.0, 0.975, b, gs,  # noqa: E731
+                                                       g, None, None, None)
+    assert f(None, 40, 0, 0, 1, 1.0, 0.975, None, None, 0, None, None, None) == NULL
     assert call(_stack(dtype=4)[0]) == DTYPE
     assert call(_stack(head_dim=96)[0]) == SHAPE
     assert call(_stack(channels=16)[0]) == SHAPE           # bf16 stacks need C % 64 == 0
@@ -261,6 +265,8 @@ def test_stack_iteration_errors(lib):
     assert call(_stack(n_layers=-1, L=1)[0]) == SHAPE
     assert call(_stack()[0], i=40) == BUDGET
     assert call(_stack()[0], m=21) == BUDGET
+    assert call(_stack()[0], p=3) == BUDGET                           # outside period must divide T
+    assert call(_stack()[0], p=0) == BUDGET
     assert call(_stack()[0], b=(ctypes.c_int32 * 2)(20, 30)) == BUDGET   # 30 does not divide 40
     assert call(_stack()[0], g=-1) == BUDGET
     assert call(_stack(h=None)[0]) == NULL

@@ -60,6 +60,23 @@ def test_active_set_bit_exact(case):
         np.testing.assert_array_equal(idx[:n].cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("N,T,budgets,margin,period", [(32760, 40, (20, 5), 4, 2), (5000, 40, (40, 10, 5), 10, 1),
+                                                       (20001, 40, (20, 10), 5, 4), (3000, 2000, (1000, 10), 100, 2)])
+def test_active_set_outside_period(N, T, budgets, margin, period):
+    b = _budgets(N, budgets, N + T)
+    idx = torch.full((N,), -7, dtype=torch.int32, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int32, device=DEV)
+    its = sorted(set(list(range(0, margin + 2)) + list(range(T - margin - 2, T))))
+    for i in its:
+        n = H.hsa_build_active_set(i32(b), T, i, margin, idx, cnt, outside_period=period)
+        ref = oracle.active_set(b, T, i, margin, period)
+        assert n == ref.size, i
+        np.testing.assert_array_equal(idx[:n].cpu().numpy(), ref)
+    with pytest.raises(H.HsaStepError) as ei:
+        H.hsa_build_active_set(i32(b), T, 0, margin, idx, cnt, outside_period=3)
+    assert ei.value.name == "HSA_STEP_ERR_BUDGET"
+
+
 def test_active_set_unaligned_budget_pointer():
     N, T = 4099, 40
     b = _budgets(N + 1, (40, 20, 10, 5), 3)

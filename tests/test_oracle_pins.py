@@ -125,11 +125,11 @@ def _load_presets():
     return rows
 
 
-def _token_step_fraction(T, alloc, window):
+def _token_step_fraction(T, alloc, window, outside_period=1):
     budget = np.concatenate([np.full(p, s) for p, s in alloc])
     assert budget.size == 100
     m = oracle.window_margin(window, T)
-    steps = sum(oracle.active_set(budget, T, i, m).size for i in range(T))
+    steps = sum(oracle.active_set(budget, T, i, m, outside_period).size for i in range(T))
     return 100.0 * steps / (budget.size * T)
 
 
@@ -154,6 +154,37 @@ def test_preset_hsa25_literal_window_reading():
     assert frac == pytest.approx(34.8, abs=1e-9)
     # without the window the preset is at 23.5% (16% at 20 steps + 84% at 5 steps over 40)
     assert _token_step_fraction(T, alloc, 100) == pytest.approx((16 * 20 + 84 * 5) / 40, abs=1e-9)
+
+
+@pytest.mark.parametrize("preset", _load_presets(), ids=lambda r: r[0])
+def test_presets_largest_budget_outside_window(preset):
+    """The other reading of the window (every token follows the largest
+    budget's schedule outside it, outside period T / s_max) reproduces every
+    printed runtime within half a point, HSA-25 included (24.8%). For the
+    presets whose largest budget is T it is the literal rule."""
+    name, T, alloc, window, runtime = preset
+    s_max = max(s for _, s in alloc)
+    frac = _token_step_fraction(T, alloc, window, T // s_max)
+    assert frac == pytest.approx(runtime, abs=0.5)
+    if s_max == T:
+        assert frac == _token_step_fraction(T, alloc, window)
+    if name == "HSA-25":
+        # 4 outside iterations with everyone active + 16 x 16% + 4 x 84% inside
+        assert frac == pytest.approx(100 * (4 + 16 * 0.16 + 4 * 0.84) / 40, abs=1e-9)
+
+
+def test_outside_period_brute_force():
+    budget = np.array([20, 5, 5, 20, 10])
+    T, m, p = 40, 4, 2
+    for i in range(T):
+        got = oracle.active_set(budget, T, i, m, p)
+        if i < m or i > T - m - 1:
+            want = np.arange(5) if i % p == 0 else np.zeros(0, np.int64)
+        else:
+            want = np.array([n for n in range(5) if i % (T // budget[n]) == 0])
+        np.testing.assert_array_equal(got, want)
+    with pytest.raises(ValueError):
+        oracle.active_set(budget, T, 0, m, 3)
 
 
 def test_window_margin_integer():
