@@ -23,11 +23,16 @@ from .hsa_oracle import (  # noqa: F401
     window_margin,
 )
 from .stack_oracle import (  # noqa: F401
+    SELECT_L1REL,
+    SELECT_NORM,
+    assign_by_key,
     assign_groups,
     boundary_gaps,
     check_group_sizes,
     gather_latent,
+    gelu_tanh,
     initial_state,
+    l1_rel,
     linear,
     refresh_period,
     rms_normalize,

@@ -26,17 +26,31 @@ Readings where the paper is silent:
   * A stack layer is the pre-norm self-attention sub-layer with its
     residual, h <- h + Attn_l(rms(h)) W_o^T, where rms(h) = h / sqrt(mean(h^2)
     + eps) per row (eps = 1e-6, no learned scale) feeds the Q/K/V
-    projections; no modulation, cross-attention or FFN. The residual stream
+    projections; no modulation. The residual stream
     is stored in the model dtype, rounded once per layer (the product and
     the add are formed exactly, then rounded). The normalized rows are not
     stored: each projection of rms(h) is formed exactly and rounded once.
     A final rms() precedes the velocity head. (Without the norms a random
     stack's residual stream grows from layer to layer and the sampled
     latent diverges within a few iterations.)
+  * Full blocks (Section 2.3: cross-attention and the feed-forward network
+    also run on the active rows only) add two pre-norm residual sub-layers
+    after self-attention: h <- h + CrossAttn(rms(h), ctx) W_oc^T, with keys
+    and values ctx W_kc^T, ctx W_vc^T of a fixed context of ctx_len rows (a
+    stand-in for the text embedding, in the model width, no mask); and
+    h <- h + gelu(rms(h) W_1^T) W_2^T with the tanh form of GELU. Every
+    materialized value (the context keys and values, the cross-attention
+    output, the FFN hidden activation) is rounded once to the model dtype.
   * Patch embedding: a linear map of the C values of a patch token (16
     latent channels times a 1x2x2 patch = 64) to d, no bias; the fp32
     latent rows are rounded once to the model dtype first. Velocity head: a
     linear map d -> C with an fp32 output. No timestep conditioning.
+  * Strategy D (Appendix B, Eq. 7) is taken as: over the initial full-budget
+    steps -- the iterations 0 .. m-1 before the caching window, where every
+    token is active -- the per-token L1_rel between consecutive fresh
+    velocities is summed (float64, channel-order sums, one division per
+    step), and after step m-1 tokens are ranked by the sum (the mean ranks
+    the same) with the same key order and group filling as below.
   * Group refresh: at the iterations i with i mod P == 0, P = lcm over the
     budgets of T/s_k -- the iterations at which every group's schedule fires,
     so every token has just produced a fresh velocity -- tokens are ranked
@@ -68,6 +82,12 @@ def gather_latent(x, idx, dtype: str) -> np.ndarray:
 
 
 RMS_EPS = 1e-6
+
+
+def gelu_tanh(x) -> np.ndarray:
+    """0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))), float64."""
+    x = np.asarray(x, np.float64)
+    return 0.5 * x * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (x + 0.044715 * x ** 3)))
 
 
 def rms_normalize(h, eps: float = RMS_EPS) -> np.ndarray:
@@ -126,15 +146,39 @@ def check_group_sizes(group_sizes, N: int, T: int | None = None) -> tuple:
     return gs
 
 
-def assign_groups(v, group_sizes) -> np.ndarray:
-    """Budgets from the velocity rows: the n_1 lowest-ranked tokens get s_1,
+def assign_by_key(keys, group_sizes) -> np.ndarray:
+    """Budgets from per-token keys: the n_1 lowest-ranked tokens get s_1,
     the next n_2 get s_2, and so on (int32[N])."""
-    v = np.asarray(v)
-    gs = check_group_sizes(group_sizes, v.shape[0])
-    rank = token_ranks(velocity_keys(v))
+    keys = np.asarray(keys, np.float64)
+    gs = check_group_sizes(group_sizes, keys.shape[0])
+    rank = token_ranks(keys)
     bounds = np.cumsum([n for _, n in gs])
     g = np.searchsorted(bounds, rank, side="right")
     return np.array([s for s, _ in gs], dtype=np.int32)[g]
+
+
+def assign_groups(v, group_sizes) -> np.ndarray:
+    """Budgets from the velocity rows, ranked by squared L2 norm."""
+    return assign_by_key(velocity_keys(v), group_sizes)
+
+
+def l1_rel(v, v_prev) -> np.ndarray:
+    """Per-token L1 relative change of the velocity (Appendix B, Eq. 7):
+    sum_c |v - v_prev| / sum_c |v|, both sums in float64 in channel order over
+    the fp32 values, then one float64 division."""
+    v = np.asarray(v, np.float64)
+    vp = np.asarray(v_prev, np.float64)
+    num = np.zeros(v.shape[0])
+    den = np.zeros(v.shape[0])
+    for c in range(v.shape[1]):
+        num = num + np.abs(v[:, c] - vp[:, c])
+        den = den + np.abs(v[:, c])
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return num / den
+
+
+SELECT_NORM = "norm"      # refresh from velocity norms where every schedule fires
+SELECT_L1REL = "l1rel"    # strategy D: mean L1_rel over the initial full-budget steps
 
 
 def boundary_gaps(keys, group_sizes) -> np.ndarray:
@@ -164,8 +208,9 @@ def refresh_period(T: int, budgets) -> int:
 
 
 def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: str) -> dict:
-    """Embedding, L pre-norm layers, final norm and velocity head for the
-    active rows.
+    """Embedding, L pre-norm layers (self-attention, and for full blocks
+    cross-attention and FFN), final norm and velocity head for the active
+    rows.
 
     xa: [|A|, C] model-dtype latent rows of the tokens idx. caches: one
     (K_hat, V_hat) pair of [N, d] arrays per layer. Returns the fp32-valued
@@ -182,6 +227,15 @@ def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: st
                              x_compact=True)
         o = round_to(attention(r["q"], r["k_cache"], r["v_cache"], heads, dh, scale), dtype)
         h = linear(o, lw["wo"], dtype, residual=h)
+        if "wq_c" in lw:  # cross-attention of the active rows to the fixed context
+            kc = linear(weights["ctx"], lw["wk_c"], dtype)
+            vc = linear(weights["ctx"], lw["wv_c"], dtype)
+            qc = linear(rms_normalize(h), lw["wq_c"], dtype)
+            oc = round_to(attention(qc, kc, vc, heads, dh, scale), dtype)
+            h = linear(oc, lw["wo_c"], dtype, residual=h)
+        if "w1" in lw:  # feed-forward network of the active rows
+            f = round_to(gelu_tanh(rms_normalize(h) @ np.asarray(lw["w1"], np.float64).T), dtype)
+            h = linear(f, lw["w2"], dtype, residual=h)
         hidden.append(h)
         new_caches.append((r["k_cache"], r["v_cache"]))
     v = linear(rms_normalize(h), weights["w_head"], "f32")
@@ -194,41 +248,68 @@ def initial_state(x0, n_layers: int, d: int, T: int) -> dict:
     x = np.asarray(x0, np.float64)
     N, C = x.shape
     return {"x": x, "v_hat": np.zeros((N, C)), "budget": np.full(N, T, dtype=np.int32),
-            "caches": [(np.zeros((N, d)), np.zeros((N, d))) for _ in range(n_layers)]}
+            "caches": [(np.zeros((N, d)), np.zeros((N, d))) for _ in range(n_layers)],
+            "v_prev": np.zeros((N, C)), "l1": np.zeros(N)}
 
 
 def stack_iteration(state: dict, weights: dict, i: int, T: int, sigmas, heads: int, dh: int,
-                    dtype: str, group_sizes=None, margin: int = 0) -> dict:
+                    dtype: str, group_sizes=None, margin: int = 0, outside_period: int = 1,
+                    selection: str = SELECT_NORM) -> dict:
     """One iteration of the multi-layer HSA sampler.
 
-    A_i from the budgets in force; the stack on the active rows (embedding of
-    the gathered latent, each layer's cache overwrite and attention, the
-    residual output projection, the velocity head); v_hat[A_i] refreshed and
-    every token advanced by Eq. 6; at refresh iterations (group_sizes given
-    and i mod P == 0) the budgets are reassigned from v_hat. Returns the new
-    state plus the active set, the fresh velocities and the hidden states.
+    A_i from the budgets in force (and the window); the stack on the active
+    rows (embedding of the gathered latent, each layer's cache overwrite and
+    attention, the residual output projection, cross-attention and FFN for
+    full blocks, the velocity head); v_hat[A_i] refreshed and every token
+    advanced by Eq. 6. Group membership (group_sizes given):
+      SELECT_NORM   at refresh iterations (i mod P == 0) the budgets are
+                    reassigned from the squared norms of v_hat;
+      SELECT_L1REL  strategy D of Appendix B: over the initial full-budget
+                    steps 0 .. m-1 (the window margin m >= 2, every token
+                    active) the L1_rel of Eq. 7 between consecutive fresh
+                    velocities is summed per token (i = 1 .. m-1; the sum
+                    ranks like the mean), and at i = m - 1 tokens are
+                    assigned by its ranking, smallest change to the smallest
+                    budget.
+    Returns the new state plus the active set, the fresh velocities and the
+    hidden states.
     """
     x = state["x"]
     N = x.shape[0]
-    idx = active_set(state["budget"], T, i, margin)
+    idx = active_set(state["budget"], T, i, margin, outside_period)
     xa = gather_latent(x, idx, dtype)
     f = stack_forward(xa, idx, weights, state["caches"], heads, dh, dtype)
     x_new, v_hat = cached_euler(x, state["v_hat"], f["v_fresh"], idx, sigmas[i], sigmas[i + 1])
     budget = state["budget"]
+    v_prev, l1 = state.get("v_prev"), state.get("l1")
     refreshed = False
     if group_sizes is not None:
         gs = check_group_sizes(group_sizes, N, T)
-        if i % refresh_period(T, [s for s, _ in gs]) == 0:
-            if idx.size != N:
-                raise ValueError("a refresh iteration must have every token active")
-            budget = assign_groups(v_hat, gs)
-            refreshed = True
+        if selection == SELECT_NORM:
+            if i % refresh_period(T, [s for s, _ in gs]) == 0:
+                if idx.size != N:
+                    raise ValueError("a refresh iteration must have every token active")
+                budget = assign_groups(v_hat, gs)
+                refreshed = True
+        elif selection == SELECT_L1REL:
+            if margin < 2 or outside_period != 1:
+                raise ValueError("strategy D needs a window margin >= 2 with every token active outside it")
+            if i < margin:
+                l1 = np.zeros(N) if i == 0 else l1 + l1_rel(v_hat, v_prev)
+                v_prev = v_hat
+                if i == margin - 1:
+                    budget = assign_by_key(l1, gs)
+                    refreshed = True
+        else:
+            raise ValueError(f"unknown selection {selection!r}")
     return {"i": i, "idx": idx, "x": x_new, "v_hat": v_hat, "caches": f["caches"], "budget": budget,
-            "refreshed": refreshed, "v_fresh": f["v_fresh"], "hidden": f["hidden"]}
+            "refreshed": refreshed, "v_fresh": f["v_fresh"], "hidden": f["hidden"], "v_prev": v_prev,
+            "l1": l1}
 
 
 def stack_trajectory(x0, weights: dict, T: int, sigmas, heads: int, dh: int, dtype: str,
-                     group_sizes=None, margin: int = 0, iterations=None, state=None) -> list:
+                     group_sizes=None, margin: int = 0, iterations=None, state=None,
+                     outside_period: int = 1, selection: str = SELECT_NORM) -> list:
     """Iterations 0..T-1 (or the first `iterations`) of the multi-layer
     sampler from initial_state (or the given state). With group_sizes None
     and every budget T this is the dense flow-matching loop. Returns one
@@ -238,7 +319,9 @@ def stack_trajectory(x0, weights: dict, T: int, sigmas, heads: int, dh: int, dty
         state = initial_state(x0, len(weights["layers"]), d, T)
     records = []
     for i in range(T if iterations is None else iterations):
-        r = stack_iteration(state, weights, i, T, sigmas, heads, dh, dtype, group_sizes, margin)
+        r = stack_iteration(state, weights, i, T, sigmas, heads, dh, dtype, group_sizes, margin,
+                            outside_period, selection)
         records.append(r)
-        state = {"x": r["x"], "v_hat": r["v_hat"], "budget": r["budget"], "caches": r["caches"]}
+        state = {"x": r["x"], "v_hat": r["v_hat"], "budget": r["budget"], "caches": r["caches"],
+                 "v_prev": r["v_prev"], "l1": r["l1"]}
     return records

@@ -37,6 +37,8 @@ class Workload:
     iters: iterations at which the workload is measured or checked.
     layers: self-attention layers of a stack workload (embedding C -> d,
     `layers` layers, velocity head d -> C); 1 for the single-block workloads.
+    ffn, ctx: for full blocks, the FFN hidden width and the context length of
+    the cross-attention (0: no such sub-layer).
     """
 
     name: str
@@ -50,6 +52,8 @@ class Workload:
     iters: tuple = ()
     C: int | None = None
     layers: int = 1
+    ffn: int = 0
+    ctx: int = 0
     notes: str = field(default="", compare=False)
 
     @property
@@ -98,6 +102,22 @@ WORKLOADS = {
         "small_stack_bf16", (2, 20, 25), 256, 2, 128, "bf16", 8,
         ((8, 0.25), (4, 0.25), (2, 0.5)), iters=(0, 1, 2), C=64, layers=4,
         notes="N=1000, d=256, 2x128, bf16, C=64, 4 layers; T=8, budgets {8:25%, 4:25%, 2:50%}",
+    ),
+    "tiny_block_f32": Workload(
+        "tiny_block_f32", (3, 10, 10), 128, 2, 64, "f32", 8,
+        ((8, 1 / 3), (4, 1 / 3), (2, 1 / 3)), iters=tuple(range(8)), C=16, layers=2, ffn=256, ctx=40,
+        notes="N=300, d=128, 2x64, fp32, C=16, 2 full blocks (FFN 256, context 40); T=8, budgets {8,4,2}",
+    ),
+    "small_block_bf16": Workload(
+        "small_block_bf16", (2, 20, 25), 256, 2, 128, "bf16", 8,
+        ((8, 0.25), (4, 0.25), (2, 0.5)), iters=(0, 1, 2), C=64, layers=3, ffn=512, ctx=77,
+        notes="N=1000, d=256, 2x128, bf16, C=64, 3 full blocks (FFN 512, context 77)",
+    ),
+    "wan1.3b_blocks": Workload(
+        "wan1.3b_blocks", (21, 30, 52), 1536, 12, 128, "bf16", 40,
+        ((40, 0.25), (20, 0.25), (10, 0.25), (5, 0.25)), iters=tuple(range(40)), C=64, layers=30, ffn=8960,
+        ctx=512,
+        notes="N=32760, d=1536, 12x128, bf16, C=64, 30 full blocks (FFN 8960, context 512); T=40, quarters",
     ),
     "wan1.3b_stack": Workload(
         "wan1.3b_stack", (21, 30, 52), 1536, 12, 128, "bf16", 40,
@@ -216,7 +236,10 @@ def draw_stack(wl: Workload, seed: int = 0, n_tokens: int | None = None, layers:
 
     x0 ~ N(0, 1) fp32 [N, C] (the latent at sigma = 1); W_embed ~ N(0, 1/C)
     [d, C]; layer weights ~ N(0, 1/d) [d, d]; W_head ~ N(0, 1/d) [C, d]; all
-    [d_out, d_in]. Weights are bf16-valued for bf16 workloads.
+    [d_out, d_in]. Weights are bf16-valued for bf16 workloads. Full-block
+    workloads then draw, from a second stream, the context ctx ~ N(0, 1)
+    [ctx_len, d] and per layer Wq_c, Wk_c, Wv_c, Wo_c ~ N(0, 1/d) [d, d],
+    W_1 ~ N(0, 1/d) [ffn, d] and W_2 ~ N(0, 1/ffn) [d, ffn].
     """
     N = wl.N if n_tokens is None else int(n_tokens)
     L = wl.layers if layers is None else int(layers)
@@ -230,7 +253,20 @@ def draw_stack(wl: Workload, seed: int = 0, n_tokens: int | None = None, layers:
         ws = [cast(_normal(rng, (d, d), 1.0 / math.sqrt(d))) for _ in range(4)]
         layer_ws.append(dict(zip(("wq", "wk", "wv", "wo"), ws)))
     w_head = cast(_normal(rng, (C, d), 1.0 / math.sqrt(d)))
-    return {"x0": x0, "w_embed": w_embed, "layers": layer_ws, "w_head": w_head}
+    out = {"x0": x0, "w_embed": w_embed, "layers": layer_ws, "w_head": w_head}
+    if wl.ctx or wl.ffn:
+        # full blocks: a second stream, so the self-attention draws above do not change
+        rng2 = np.random.default_rng([seed, 0xB10C])
+        if wl.ctx:
+            out["ctx"] = cast(_normal(rng2, (wl.ctx, d)))
+        for lw in layer_ws:
+            if wl.ctx:
+                for k in ("wq_c", "wk_c", "wv_c", "wo_c"):
+                    lw[k] = cast(_normal(rng2, (d, d), 1.0 / math.sqrt(d)))
+            if wl.ffn:
+                lw["w1"] = cast(_normal(rng2, (wl.ffn, d), 1.0 / math.sqrt(d)))
+                lw["w2"] = cast(_normal(rng2, (d, wl.ffn), 1.0 / math.sqrt(wl.ffn)))
+    return out
 
 
 def draw_stack_state(wl: Workload, seed: int, n_tokens: int | None = None, layers: int | None = None):

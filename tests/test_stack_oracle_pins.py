@@ -152,6 +152,16 @@ def _torch_iteration(x, v_hat, caches, wts, idx, heads, dh, dsig, dtype="f32"):
         o = F.scaled_dot_product_attention(split(q), split(K), split(V))
         o = rnd(o.transpose(0, 1).reshape(q.shape[0], heads * dh))
         h = rnd(F.linear(o, D(lw["wo"])) + h)
+        if "wq_c" in lw:
+            ctx = D(wts["ctx"])
+            kc, vc = rnd(F.linear(ctx, D(lw["wk_c"]))), rnd(F.linear(ctx, D(lw["wv_c"])))
+            qc = rnd(F.linear(norm(h), D(lw["wq_c"])))
+            oc = F.scaled_dot_product_attention(split(qc), split(kc), split(vc))
+            oc = rnd(oc.transpose(0, 1).reshape(qc.shape[0], heads * dh))
+            h = rnd(F.linear(oc, D(lw["wo_c"])) + h)
+        if "w1" in lw:
+            f = rnd(F.gelu(F.linear(norm(h), D(lw["w1"])), approximate="tanh"))
+            h = rnd(F.linear(f, D(lw["w2"])) + h)
         new_caches.append((K.numpy(), V.numpy()))
     v = f32(F.linear(norm(h), D(wts["w_head"])))
     vh = D(v_hat).clone()
@@ -160,9 +170,10 @@ def _torch_iteration(x, v_hat, caches, wts, idx, heads, dh, dsig, dtype="f32"):
     return x_new.numpy(), vh.numpy(), v.numpy(), new_caches
 
 
+@pytest.mark.parametrize("name", ["tiny_stack_f32", "tiny_block_f32"])
 @pytest.mark.parametrize("iteration", [1, 2, 4])  # 33%, 67% and 100% of the tokens active
-def test_stack_iteration_matches_torch(iteration):
-    wl = synth.WORKLOADS["tiny_stack_f32"]
+def test_stack_iteration_matches_torch(iteration, name):
+    wl = synth.WORKLOADS[name]
     wts = synth.draw_stack(wl, seed=11)
     st = synth.draw_stack_state(wl, seed=12)
     budget = synth.assign_budgets(st["v_hat"], wl.groups)
@@ -183,12 +194,13 @@ def test_stack_iteration_matches_torch(iteration):
         np.testing.assert_allclose(vv, vt, **tol)
 
 
+@pytest.mark.parametrize("name", ["small_stack_bf16", "small_block_bf16"])
 @pytest.mark.parametrize("iteration", [1, 2])
-def test_bf16_stack_iteration_matches_torch(iteration):
+def test_bf16_stack_iteration_matches_torch(iteration, name):
     """Same check with bf16 storage: the two sides round at the same points,
     so all but a few values (where float64 summation order decides a bf16
     rounding) agree to float64 precision."""
-    wl = synth.WORKLOADS["small_stack_bf16"]
+    wl = synth.WORKLOADS[name]
     wts = synth.draw_stack(wl, seed=21, n_tokens=384, layers=2)
     st = synth.draw_stack_state(wl, seed=22, n_tokens=384, layers=2)
     budget = synth.assign_budgets(st["v_hat"], wl.groups)
@@ -351,9 +363,78 @@ def test_hsa_loop_zero_attention_telescopes_per_token():
         np.testing.assert_allclose(recs[i0 + P - 1]["x"], x, rtol=0, atol=2e-5 * np.abs(x).max())
 
 
+def test_gelu_tanh_matches_torch():
+    x = np.linspace(-12, 12, 20001)
+    t = F.gelu(torch.from_numpy(x), approximate="tanh").numpy()
+    np.testing.assert_allclose(oracle.gelu_tanh(x), t, rtol=1e-14, atol=1e-15)
+
+
 def test_rms_normalize_matches_torch():
     rng = np.random.default_rng(9)
     h = rng.standard_normal((50, 96)) * rng.uniform(0.01, 100, size=(50, 1))
     t = F.rms_norm(torch.from_numpy(h), (96,), eps=1e-6).numpy()
     np.testing.assert_allclose(oracle.rms_normalize(h), t, rtol=1e-13, atol=0)
     np.testing.assert_allclose(np.mean(oracle.rms_normalize(h) ** 2, axis=1), 1.0, rtol=1e-4)
+
+
+# ---------------------------------------------------------------------------
+# Strategy D: L1 relative change of the velocity (Appendix B, Eq. 7)
+# ---------------------------------------------------------------------------
+
+
+def test_l1_rel_exact_on_integers_and_matches_numpy():
+    from fractions import Fraction
+    rng = np.random.default_rng(12)
+    v = rng.integers(-9, 10, size=(40, 7)).astype(np.float32)
+    vp = rng.integers(-9, 10, size=(40, 7)).astype(np.float32)
+    v[3] = 0.0  # zero velocity: 0/0 or x/0
+    got = oracle.l1_rel(v, vp)
+    for n in range(40):
+        num = sum(abs(int(a) - int(b)) for a, b in zip(v[n], vp[n]))
+        den = sum(abs(int(a)) for a in v[n])
+        if den == 0:
+            assert np.isnan(got[n]) if num == 0 else np.isinf(got[n])
+        else:
+            assert got[n] == float(Fraction(num, den))  # one correctly rounded division
+    a = rng.standard_normal((500, 64)).astype(np.float32)
+    b = rng.standard_normal((500, 64)).astype(np.float32)
+    ref = np.linalg.norm(a.astype(np.float64) - b, 1, axis=1) / np.linalg.norm(a.astype(np.float64), 1, axis=1)
+    np.testing.assert_allclose(oracle.l1_rel(a, b), ref, rtol=1e-14)
+
+
+@pytest.mark.parametrize("margin", [2, 3])
+def test_strategy_d_ranks_mean_l1_rel_of_initial_steps(margin):
+    wl = synth.WORKLOADS["tiny_stack_f32"]
+    wts = synth.draw_stack(wl, seed=3)
+    sizes = synth.group_sizes(wl.N, wl.groups)
+    recs = oracle.stack_trajectory(wts["x0"], wts, wl.T, synth.linear_sigmas(wl.T), wl.heads, wl.dh, "f32",
+                                   group_sizes=sizes, margin=margin, selection=oracle.SELECT_L1REL)
+    vs = [r["v_fresh"] for r in recs[:margin]]
+    assert all(r["idx"].size == wl.N for r in recs[:margin])
+    mean = np.mean([np.linalg.norm(vs[i] - vs[i - 1], 1, axis=1) / np.linalg.norm(vs[i], 1, axis=1)
+                    for i in range(1, margin)], axis=0)
+    order = np.argsort(mean, kind="stable")
+    want = np.empty(wl.N, np.int32)
+    start = 0
+    for s, n in sizes:
+        want[order[start:start + n]] = s
+        start += n
+    b = recs[margin - 1]["budget"]
+    assert [r["refreshed"] for r in recs] == [i == margin - 1 for i in range(wl.T)]
+    np.testing.assert_array_equal(b, want)
+    assert oracle.boundary_gaps(recs[margin - 1]["l1"], sizes).min() > 1e-6
+    assert np.all(np.diff(b[np.argsort(mean)]) >= 0)  # larger change, never a smaller budget
+    for r in recs[margin:]:
+        np.testing.assert_array_equal(r["budget"], b)
+        np.testing.assert_array_equal(r["idx"], oracle.active_set(b, wl.T, r["i"], margin))
+
+
+def test_strategy_d_needs_initial_full_steps():
+    wl = synth.WORKLOADS["tiny_stack_f32"]
+    wts = synth.draw_stack(wl, seed=3)
+    sizes = synth.group_sizes(wl.N, wl.groups)
+    for margin, period in ((1, 1), (0, 1), (2, 2)):
+        with pytest.raises(ValueError):
+            oracle.stack_trajectory(wts["x0"], wts, wl.T, synth.linear_sigmas(wl.T), wl.heads, wl.dh, "f32",
+                                    group_sizes=sizes, margin=margin, outside_period=period,
+                                    selection=oracle.SELECT_L1REL, iterations=1)
