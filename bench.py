@@ -62,6 +62,8 @@ def parse():
     p.add_argument("--no-end-to-end", action="store_true",
                    help="skip the 30-layer sampling loops (HSA vs dense, T = 40)")
     p.add_argument("--end-to-end-only", action="store_true", help="run only the 30-layer sampling loops")
+    p.add_argument("--no-blocks", action="store_true",
+                   help="skip the full-block (cross-attention + FFN) loops with the Appendix C presets")
     p.add_argument("--summarize", metavar="DIR", default=None,
                    help="print a text summary of the rocprofv3 csv output under DIR and exit")
     p.add_argument("--write-traffic", metavar="DIR", default=None,
@@ -330,76 +332,120 @@ def euler_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
             "bytes": nbytes, "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
-def stack_flops(n_active, N, d, C, layers):
+def stack_flops(n_active, N, d, C, layers, ffn=0, ctx=0):
     """Matrix-product FLOPs of one stack pass over n_active rows: embedding,
     per layer Q/K/V, attention against N cached rows and the output
-    projection, velocity head."""
+    projection (plus, for full blocks, cross-attention to ctx rows and the
+    FFN), velocity head."""
     per_layer = gemm_flops(n_active, d) + attention_flops(n_active, N, d)
+    if ctx:
+        per_layer += 4.0 * n_active * d * d + attention_flops(n_active, ctx, d)
+    if ffn:
+        per_layer += 4.0 * n_active * d * ffn
     return 2.0 * n_active * C * d * 2 + layers * per_layer
 
 
-def end_to_end(dev, name="wan1.3b_stack"):
-    """Whole T = 40 sampling loops of the 30-layer Wan-1.3B-shaped stack on the
-    same seed and weights: the HSA loop (budgets {40, 20, 10, 5} on quarters of
-    the tokens, groups refreshed from velocity norms where every schedule
-    fires) and the dense loop (every token at every iteration: flow matching
-    with T = 40). Each loop is timed on the host clock between two device
-    synchronizations, so it includes the per-iteration read-back of |A_i|."""
+def end_to_end(dev, name="wan1.3b_stack", presets=False):
+    """Whole T = 40 sampling loops of a 30-layer Wan-1.3B-shaped stack on the
+    same seed and weights: the dense loop (every token at every iteration:
+    flow matching with T = 40) and the HSA loop with budgets {40, 20, 10, 5}
+    on quarters of the tokens, groups refreshed from velocity norms where
+    every schedule fires; with presets, also the Appendix C presets with
+    their windows (strategy D from L1_rel for HSA-75A/75B/50, random
+    allocation for HSA-25). Each loop is timed on the host clock between two
+    device synchronizations, so it includes the per-iteration read-back of
+    |A_i|."""
     import torch
 
     import synth
+    from paper_2605_06892_amd import hsa_step as H
+    from paper_2605_06892_amd import layer as LY
     from paper_2605_06892_amd import stack as S
 
     wl = synth.WORKLOADS[name]
     N, C, L, d, T = wl.N, wl.euler_channels, wl.layers, wl.d, wl.T
     t_draw = time.perf_counter()
     wts = synth.draw_stack(wl, seed=0)
-    b = S.StackBuffers.allocate(N, C, L, wl.heads, wl.dh, torch.bfloat16, device=dev)
-    b.w_embed.copy_(synth.bf16_tensor(wts["w_embed"]))
-    b.w_head.copy_(synth.bf16_tensor(wts["w_head"]))
+    b = S.StackBuffers.allocate(N, C, L, wl.heads, wl.dh, torch.bfloat16, device=dev, ffn=wl.ffn, ctx=wl.ctx)
+    bf = synth.bf16_tensor
+    b.w_embed.copy_(bf(wts["w_embed"]))
+    b.w_head.copy_(bf(wts["w_head"]))
     for dst, lw in zip(b.layers, wts["layers"]):
         for t, k in zip(dst, ("wq", "wk", "wv", "wo")):
-            t.copy_(synth.bf16_tensor(lw[k]))
+            t.copy_(bf(lw[k]))
+    if wl.ctx:
+        for dst, lw in zip(b.cross, wts["layers"]):
+            dst[0].copy_(bf(lw["wq_c"]))
+            dst[1].copy_(bf(lw["wo_c"]))
+        ctx = bf(wts["ctx"]).to(dev)
+        b.set_context(ctx, [bf(lw["wk_c"]).to(dev) for lw in wts["layers"]],
+                      [bf(lw["wv_c"]).to(dev) for lw in wts["layers"]])
+    if wl.ffn:
+        for dst, lw in zip(b.ffn, wts["layers"]):
+            dst[0].copy_(bf(lw["w1"]))
+            dst[1].copy_(bf(lw["w2"]))
     x0 = torch.from_numpy(wts["x0"]).to(dev)
     del wts
     t_draw = time.perf_counter() - t_draw
-    sizes = synth.group_sizes(N, wl.groups)
     sig = synth.linear_sigmas(T)
 
-    def reset():
+    def loop(groups, budget0=None, margin=0, outside_period=1, selection=H.SELECT_VELOCITY_NORM, iterations=T):
         b.x.copy_(x0)
         b.v_hat.zero_()
-        b.budget.fill_(T)
+        if budget0 is None:
+            b.budget.fill_(T)
+        else:
+            b.budget.copy_(torch.from_numpy(budget0))
         torch.cuda.synchronize()
-
-    def loop(groups, iterations=T):
-        reset()
         t0 = time.perf_counter()
-        res = S.run(b, T, sig, groups, iterations=iterations)
+        res = S.run(b, T, sig, groups, margin=margin, iterations=iterations, outside_period=outside_period,
+                    selection=selection)
         torch.cuda.synchronize()
-        return (time.perf_counter() - t0) * 1e3, res
+        ms = (time.perf_counter() - t0) * 1e3
+        fl = sum(stack_flops(n, N, d, C, L, wl.ffn, wl.ctx) for n, _ in res)
+        return ms, {"token_step_fraction": round(sum(n for n, _ in res) / (N * T), 4),
+                    "refreshes": int(sum(r for _, r in res)), "tflops": round(fl / (ms * 1e-3) / 1e12, 1),
+                    "final_latent_finite": bool(torch.isfinite(b.x).all())}
 
-    loop(sizes, 2)  # warm-up: a dense and a partial iteration
-    dense_ms, dres = loop(None)
-    dense_finite = bool(torch.isfinite(b.x).all())
-    hsa_ms, hres = loop(sizes)
-    hsa_finite = bool(torch.isfinite(b.x).all())
-    dense_fl = sum(stack_flops(n, N, d, C, L) for n, _ in dres)
-    hsa_fl = sum(stack_flops(n, N, d, C, L) for n, _ in hres)
-    return {
-        "workload": (f"{name}: {L} layers, N={N} ({'x'.join(map(str, wl.grid))}), d={d} ({wl.heads}x{wl.dh}), "
-                     f"C={C} fp32 latent, bf16 model, T={T}, budgets {{40,20,10,5}} on quarters by velocity-norm "
-                     f"rank, refreshed every {math.lcm(*[T // s for s, _ in sizes])} iterations"),
+    sizes = synth.group_sizes(N, wl.groups)
+    loop(sizes, iterations=2)  # warm-up: a dense and a partial iteration
+    dense_ms, dense = loop(None)
+    hsa_ms, hsa = loop(sizes)
+    out = {
+        "workload": (f"{name}: {L} {'full blocks (FFN ' + str(wl.ffn) + ', context ' + str(wl.ctx) + ')' if wl.ffn else 'layers'}, "
+                     f"N={N} ({'x'.join(map(str, wl.grid))}), d={d} ({wl.heads}x{wl.dh}), C={C} fp32 latent, bf16 model, "
+                     f"T={T}, budgets {{40,20,10,5}} on quarters by velocity-norm rank, refreshed every "
+                     f"{math.lcm(*[T // s for s, _ in sizes])} iterations"),
         "dense_T40_ms": round(dense_ms, 1),
         "hsa_ms": round(hsa_ms, 1),
         "runtime_vs_dense": round(hsa_ms / dense_ms, 4),
-        "token_step_fraction": round(sum(n for n, _ in hres) / (N * T), 4),
-        "refreshes": int(sum(r for _, r in hres)),
-        "final_latents_finite": dense_finite and hsa_finite,
-        "dense_tflops": round(dense_fl / (dense_ms * 1e-3) / 1e12, 1),
-        "hsa_tflops": round(hsa_fl / (hsa_ms * 1e-3) / 1e12, 1),
+        "token_step_fraction": hsa["token_step_fraction"],
+        "refreshes": hsa["refreshes"],
+        "final_latents_finite": dense["final_latent_finite"] and hsa["final_latent_finite"],
+        "dense_tflops": dense["tflops"],
+        "hsa_tflops": hsa["tflops"],
         "setup_s": round(t_draw, 1),
     }
+    if presets:
+        for pname, pre in synth.PRESETS.items():
+            psizes = synth.group_sizes(N, pre["groups"])
+            m = LY.window_margin(pre["window"], T)
+            if pre["strategy"] == "D":
+                ms, r = loop(psizes, margin=m, selection=H.SELECT_L1_REL)
+                how = f"strategy D (L1_rel over iterations 0-{m - 1})"
+            else:  # random allocation, fixed for the trajectory
+                budget0 = synth.random_budgets(N, pre["groups"], seed=0)
+                ms, r = loop(None, budget0=budget0, margin=m)
+                how = "random allocation"
+            r.update({"ms": round(ms, 1), "runtime_vs_dense": round(ms / dense_ms, 4), "selection": how,
+                      "window_margin": m, "paper_runtime": pre["printed_runtime"]})
+            out[pname] = r
+            s_max = max(g[0] for g in pre["groups"])
+            if s_max < T and pre["strategy"] != "D":  # the other window reading (strategy D needs period 1)
+                ms, r2 = loop(None, budget0=budget0, margin=m, outside_period=T // s_max)
+                r2.update({"ms": round(ms, 1), "runtime_vs_dense": round(ms / dense_ms, 4)})
+                out[pname]["outside_period_T_over_smax"] = r2
+    return out
 
 
 def cpu_baseline(wl, blk, budget, it):
@@ -460,7 +506,11 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     if args.end_to_end_only:
-        print(json.dumps({"end_to_end": end_to_end(dev)}))
+        out = {"end_to_end": end_to_end(dev)}
+        if not args.no_blocks:
+            torch.cuda.empty_cache()
+            out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True)
+        print(json.dumps(out))
         return
     wl = synth.WORKLOADS[args.workload]
     sigmas = synth.linear_sigmas(wl.T)
@@ -556,6 +606,9 @@ def main():
     if not args.no_end_to_end:
         out["end_to_end"] = end_to_end(dev)
         torch.cuda.empty_cache()
+        if not args.no_blocks:
+            out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True)
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, blk, budget, args.iteration)
     print(json.dumps(out))

@@ -68,6 +68,12 @@ typedef enum hsa_step_status {
 
 typedef enum hsa_step_dtype { HSA_STEP_F32 = 0, HSA_STEP_BF16 = 1 } hsa_step_dtype;
 
+/* How a multi-layer loop sets group membership (Appendix B). */
+typedef enum hsa_step_selection {
+  HSA_SELECT_VELOCITY_NORM = 0, /* refresh from squared velocity norms where every schedule fires */
+  HSA_SELECT_L1_REL = 1         /* strategy D: summed L1_rel (Eq. 7) over the initial full steps */
+} hsa_step_selection;
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* hsa_step_status_string(int status);
 
@@ -227,23 +233,26 @@ int hsa_row_rms_scale(int dtype, const void* x, int32_t n_rows, int32_t d, float
 
 /*
  * Compact row map of the stack (the embedding, the residual output
- * projection of a layer, the velocity head; Section 2.3: after attention
- * every per-token computation runs on the active rows only):
- *   y[m] = s[m] (x[m] W^T) (+ residual[m]),  m < n_rows,
- * with s = row_scale (1 if NULL), accumulated in fp32 and rounded once to
- * out_dtype. With row_scale from hsa_row_rms_scale(x) this is rms(x) W^T.
+ * projection of a layer, the FFN, the velocity head; Section 2.3: after
+ * attention every per-token computation runs on the active rows only):
+ *   y[m] = act(s[m] (x[m] W^T)) (+ residual[m]),  m < n_rows,
+ * with s = row_scale (1 if NULL) and act the tanh GELU 0.5 z (1 + tanh(
+ * sqrt(2/pi) (z + 0.044715 z^3))) if gelu != 0, else the identity;
+ * accumulated in fp32 and rounded once to out_dtype. With row_scale from
+ * hsa_row_rms_scale(x) the product is rms(x) W^T.
  *   x          [n_rows, d_in] dtype     w  [d_out, d_in] dtype
  *   row_scale  NULL or [n_rows] fp32
  *   residual   NULL or [n_rows, d_out] out_dtype; it may be y itself (in-place
  *              h += ...), but must not overlap y otherwise
  *   y          [n_rows, d_out] out_dtype
  * out_dtype is dtype, or HSA_STEP_F32 with dtype HSA_STEP_BF16 (then no
- * residual). bf16 inputs need d_in % 64 == 0, d_out % 4 == 0 and 16-byte
- * aligned pointers. y must not overlap x, w or row_scale.
+ * residual and no GELU); GELU takes no residual. bf16 inputs need
+ * d_in % 64 == 0, d_out % 4 == 0 and 16-byte aligned pointers. y must not
+ * overlap x, w or row_scale.
  */
 int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, const void* w,
-               int32_t d_out, const float* row_scale, const void* residual, int out_dtype,
-               void* y, hipStream_t stream);
+               int32_t d_out, const float* row_scale, const void* residual, int32_t gelu,
+               int out_dtype, void* y, hipStream_t stream);
 
 /* Bytes of device workspace hsa_assign_budgets needs: 8 * n_tokens. */
 size_t hsa_assign_budgets_workspace_bytes(int64_t n_tokens);
@@ -272,6 +281,28 @@ int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channels, int32
                        const int32_t* group_budget, const int64_t* group_size, int32_t n_groups,
                        int32_t* budget, void* workspace, size_t workspace_bytes,
                        hipStream_t stream);
+
+/*
+ * Strategy D accumulation (Appendix B, Eq. 7), for every token t:
+ *   first != 0:  acc[t] = 0;
+ *   first == 0:  acc[t] += (sum_c |v[t][c] - v_prev[t][c]|) / (sum_c |v[t][c]|),
+ *                both sums in float64 in channel order, one float64 division
+ *                (0/0 gives NaN, x/0 infinity);
+ *   then v_prev[t] = v[t].
+ *   v, v_prev  [n_tokens, channels] fp32     acc  [n_tokens] float64
+ * v_prev and acc must not overlap v or each other.
+ */
+int hsa_l1_rel_accumulate(const float* v, float* v_prev, int64_t n_tokens, int32_t channels,
+                          double* acc, int32_t first, hipStream_t stream);
+
+/*
+ * Group assignment from given per-token keys (float64), with the rank,
+ * key order and group table of hsa_assign_budgets (which uses the squared
+ * velocity norms as keys). keys must not overlap budget.
+ */
+int hsa_assign_budgets_by_key(const double* keys, int64_t n_tokens, int32_t T,
+                              const int32_t* group_budget, const int64_t* group_size,
+                              int32_t n_groups, int32_t* budget, hipStream_t stream);
 
 /*
  * Device state and caller-owned scratch of one stack. Every pointer except
@@ -304,6 +335,17 @@ typedef struct hsa_stack {
   float* v_fresh;                 /* scratch [N, C] fp32 */
   void* keys;                     /* scratch 8 * N bytes (used by refresh iterations) */
   float* row_scale;               /* scratch [N] fp32: per-row RMS factors */
+  /* full blocks (Section 2.3: cross-attention and FFN of the active rows) */
+  int32_t ffn_dim;                /* 0: no FFN sub-layer; else the hidden width (bf16: % 64 == 0) */
+  int32_t ctx_len;                /* 0: no cross-attention; else the context rows */
+  const void* const* w_cross;     /* HOST array of 4 * n_layers pointers when ctx_len > 0:
+                                     Wq_c, Wo_c ([d, d]), then the context keys K_c = ctx Wk_c^T
+                                     and values V_c = ctx Wv_c^T ([ctx_len, d], computed once by
+                                     the caller, e.g. with hsa_linear) of layer 0, then layer 1... */
+  const void* const* w_ffn;       /* HOST array of 2 * n_layers pointers when ffn_dim > 0:
+                                     W1 [ffn_dim, d], W2 [d, ffn_dim] of each layer */
+  void* f;                        /* scratch [N, ffn_dim] dtype when ffn_dim > 0 */
+  float* v_prev;                  /* scratch [N, C] fp32 (HSA_SELECT_L1_REL) */
 } hsa_stack;
 
 /*
@@ -313,16 +355,25 @@ typedef struct hsa_stack {
  *      stream synchronization per iteration);
  *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of rms(h), cache rows
  *      A_i overwritten, attention of the |A_i| queries against all N cached
- *      rows (scale 1/sqrt(head_dim)), h <- h + O Wo^T; then
- *      v_fresh = rms(h) W_head^T;
+ *      rows (scale 1/sqrt(head_dim)), h <- h + O Wo^T; with ctx_len > 0
+ *      h <- h + CrossAttn(rms(h) Wq_c^T, K_c, V_c) Wo_c^T; with ffn_dim > 0
+ *      h <- h + gelu(rms(h) W1^T) W2^T; then v_fresh = rms(h) W_head^T;
  *   3. v_hat[A_i] = v_fresh, then x <- x + v_hat (sigma_next - sigma_i) for
  *      all tokens (Eq. 6, as hsa_cached_euler);
- *   4. if n_groups > 0 and i is a multiple of P = lcm over the group budgets
- *      of T / s_k (the iterations where every group's schedule fires), the
- *      budgets are reassigned from v_hat as hsa_assign_budgets; they hold
- *      from iteration i + 1. A refresh iteration where not every token is
- *      active returns HSA_STEP_ERR_BUDGET after step 3 (the budgets in force
- *      did not come from the group table).
+ *   4. group membership, if n_groups > 0:
+ *      HSA_SELECT_VELOCITY_NORM: if i is a multiple of P = lcm over the group
+ *        budgets of T / s_k (the iterations where every group's schedule
+ *        fires), the budgets are reassigned from v_hat as hsa_assign_budgets.
+ *        A refresh iteration where not every token is active returns
+ *        HSA_STEP_ERR_BUDGET after step 3 (the budgets in force did not come
+ *        from the group table).
+ *      HSA_SELECT_L1_REL (strategy D; needs margin >= 2 and outside_period
+ *        1): at iterations i < margin (every token active) the fresh
+ *        velocities feed hsa_l1_rel_accumulate into the keys scratch (first
+ *        at i = 0; the keys buffer carries the sums from one call to the
+ *        next), and at i = margin - 1 the budgets are assigned from the sums
+ *        as hsa_assign_budgets_by_key.
+ *      New budgets hold from iteration i + 1.
  * Iteration 0 activates every token whatever the budgets are, which fills
  * every cache and the velocity cache; later iterations read cache rows
  * written earlier. n_groups == 0 and every budget T is the dense loop.
@@ -333,7 +384,8 @@ typedef struct hsa_stack {
 int hsa_stack_iteration(const hsa_stack* stack, int32_t T, int32_t iter, int32_t margin,
                         int32_t outside_period, float sigma_i, float sigma_next,
                         const int32_t* group_budget, const int64_t* group_size, int32_t n_groups,
-                        int32_t* n_active_host, int32_t* refreshed_host, hipStream_t stream);
+                        int32_t selection, int32_t* n_active_host, int32_t* refreshed_host,
+                        hipStream_t stream);
 
 #ifdef __cplusplus
 }

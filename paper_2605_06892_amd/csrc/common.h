@@ -30,6 +30,12 @@ __device__ __forceinline__ int xcd_contiguous(int L, int total) {
 // Round fp32 to bf16, nearest-even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ bf16x4 to_bf16x4(f32x4 v) { return __builtin_convertvector(v, bf16x4); }
 
+// 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  return 0.5f * x * (1.f + tanhf(k0 * fmaf(0.044715f * x, x * x, x)));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
@@ -55,6 +61,7 @@ hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int 
 // outputs sharing A. a_rows / c_rows may be null (identity); rows whose index is
 // outside [0, a_limit) / [0, c_limit) are skipped. Row m of the product may be
 // scaled by row_scale[m] (an RMS normalization of A's rows folded into the
+// product), then optionally passed through the tanh GELU (the FFN's first
 // product). Single-output products may add a residual R indexed like C
 // (R[crow(m)][n], same leading dimension; R may be C itself) before the one
 // rounding, and a bf16 product may store fp32.
@@ -75,6 +82,7 @@ struct RowGemm {
   const void* residual;    // n_out == 1 only; in the output's dtype
   int c_f32;               // bf16 inputs, fp32 output (no residual)
   const float* row_scale;  // null, or one factor per product row m < M
+  int gelu;                // apply the tanh GELU after the row scale (no residual)
 };
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s);
 
@@ -121,6 +129,15 @@ struct GroupTable {
   int32_t budget[kMaxGroups];
   int64_t end[kMaxGroups];
 };
+
+// budget[t] from the rank of (keys[t], t), keys compared as bit patterns.
+hipError_t launch_rank_budgets(const double* keys, long n_tokens, const GroupTable& tab,
+                               int32_t* budget, hipStream_t s);
+
+// Strategy D: acc[t] += |v[t] - v_prev[t]|_1 / |v[t]|_1 (acc[t] = 0 when
+// first), then v_prev[t] = v[t].
+hipError_t launch_l1_rel(const float* v, float* v_prev, long n_tokens, int channels, double* acc,
+                         bool first, hipStream_t s);
 
 // Group refresh: keys[t] = squared L2 norm of v[t] (float64, channel order),
 // then budget[t] from the rank of (keys[t], t).

@@ -44,8 +44,9 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 // Epilogues (after the optional per-row scale): bf16 store, bf16 store of
-// (product + bf16 residual) rounded once, fp32 store.
-enum Epilogue { kEpiBf16 = 0, kEpiBf16Residual = 1, kEpiF32 = 2 };
+// (product + bf16 residual) rounded once, fp32 store, bf16 store of the tanh
+// GELU of the product.
+enum Epilogue { kEpiBf16 = 0, kEpiBf16Residual = 1, kEpiF32 = 2, kEpiBf16Gelu = 3 };
 
 // NOUT (1 or 3) is the number of outputs sharing A; it is a template
 // parameter so the Q/K/V projection and the output projection are distinct
@@ -201,6 +202,10 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
                   *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + obase + n);
               v += __builtin_convertvector(r, f32x4);
             }
+            if constexpr (EPI == kEpiBf16Gelu) {
+#pragma unroll
+              for (int u = 0; u < 4; ++u) v[u] = gelu_tanh(v[u]);
+            }
             *reinterpret_cast<bf16x4*>(static_cast<bf16*>(oz.C) + obase + n) = to_bf16x4(v);
           }
         }
@@ -226,6 +231,7 @@ hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   // would otherwise leave CUs idle in the last round of workgroups.
   if (g.n_out == 3) return launch<256, 256, 2, 3, kEpiBf16>(g, s);
   if (g.c_f32) return launch<256, 128, 4, 1, kEpiF32>(g, s);
+  if (g.gelu) return launch<256, 128, 4, 1, kEpiBf16Gelu>(g, s);
   if (g.residual) return launch<256, 128, 4, 1, kEpiBf16Residual>(g, s);
   return launch<256, 128, 4, 1, kEpiBf16>(g, s);
 }

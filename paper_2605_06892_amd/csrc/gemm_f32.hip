@@ -4,8 +4,8 @@
 // Plain FMA tiling: a 64 x 64 output tile per 256-thread workgroup, each
 // thread accumulating a 4 x 4 block, K step 16 staged through LDS. Arbitrary
 // M, Nc and K (ragged edges are masked). An optional per-row scale multiplies
-// each product row, and an optional fp32 residual, indexed like the output, is
-// added before the store.
+// each product row, an optional tanh GELU follows, and an optional fp32
+// residual, indexed like the output, is added before the store.
 #include "common.h"
 
 namespace hsa {
@@ -84,7 +84,8 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
       const int n = tn * TN + tx * 4 + j;
       if (n < g.Nc) {
         const long e = (long)crow * g.ldc + n;
-        const float v = g.row_scale ? acc[i][j] * rs : acc[i][j];
+        float v = g.row_scale ? acc[i][j] * rs : acc[i][j];
+        if (g.gelu) v = gelu_tanh(v);
         C[e] = R ? v + R[e] : v;
       }
     }

@@ -12,6 +12,10 @@
 //     made the canonical positive NaN, above every number). The n_1 lowest
 //     ranks get budget s_1, the next n_2 get s_2, and so on.
 //
+//   * l1_rel_accumulate: strategy D (Appendix B, Eq. 7): per token, the sum
+//     over the initial full-budget steps of |v_i - v_{i-1}|_1 / |v_i|_1, the
+//     two L1 norms summed in float64 in channel order, one float64 division
+//     per step; v_{i-1} is kept in a token-major copy.
 //   * row_rms_scale: 1 / sqrt(mean(h^2) + eps) of every compact hidden row, the
 //     RMS normalization before each layer's Q/K/V projections and before the
 //     velocity head. A per-row factor commutes with the projection, so the
@@ -78,6 +82,34 @@ __device__ __forceinline__ double canonical_key(double acc) {
   return acc != acc ? __longlong_as_double(0x7FF8000000000000LL) : acc;
 }
 
+// bit pattern of a key, NaNs made the canonical positive NaN
+__device__ __forceinline__ unsigned long long key_bits(unsigned long long k) {
+  const unsigned long long e = 0x7FF0000000000000ull;
+  return ((k & e) == e && (k & 0x000FFFFFFFFFFFFFull)) ? 0x7FF8000000000000ull : k;
+}
+
+__global__ __launch_bounds__(kThreads) void l1_rel_accumulate(const float* __restrict__ v,
+                                                              float* __restrict__ v_prev, long n,
+                                                              int channels, double* __restrict__ acc,
+                                                              int first) {
+  for (long t = blockIdx.x * (long)kThreads + threadIdx.x; t < n; t += (long)gridDim.x * kThreads) {
+    const float* row = v + t * channels;
+    float* prev = v_prev + t * channels;
+    if (first) {
+      acc[t] = 0.0;
+    } else {
+      double num = 0.0, den = 0.0;
+      for (int c = 0; c < channels; ++c) {
+        const double a = row[c], b = prev[c];
+        num = num + fabs(a - b);
+        den = den + fabs(a);
+      }
+      acc[t] = acc[t] + num / den;
+    }
+    for (int c = 0; c < channels; ++c) prev[c] = row[c];
+  }
+}
+
 // one thread per token; channel order is the summation order
 __global__ __launch_bounds__(kThreads) void velocity_keys_vec(const f32x4* __restrict__ v, long n,
                                                               int vpr, double* __restrict__ keys) {
@@ -121,12 +153,12 @@ __global__ __launch_bounds__(kThreads) void rank_budgets(const unsigned long lon
   __shared__ int partial[kThreads / kWave][kRankTokens];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int t = blockIdx.x * kRankTokens + lane;
-  const unsigned long long kt = t < n ? keys[t] : 0ull;
+  const unsigned long long kt = t < n ? key_bits(keys[t]) : 0ull;
   int count = 0;
   for (int m0 = 0; m0 < n; m0 += kRankTile) {
     const int cnt = min(kRankTile, n - m0);
     __syncthreads();  // the previous tile is no longer read
-    for (int e = threadIdx.x; e < cnt; e += kThreads) tile[e] = keys[m0 + e];
+    for (int e = threadIdx.x; e < cnt; e += kThreads) tile[e] = key_bits(keys[m0 + e]);
     __syncthreads();
     const int lo = wave * (kRankTile / 4);
     const int hi = min(lo + kRankTile / 4, cnt);
@@ -232,6 +264,23 @@ hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active
   return hipGetLastError();
 }
 
+hipError_t launch_rank_budgets(const double* keys, long n_tokens, const GroupTable& tab,
+                               int32_t* budget, hipStream_t s) {
+  if (n_tokens <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n_tokens + kRankTokens - 1) / kRankTokens);
+  hipLaunchKernelGGL(rank_budgets, dim3(blocks), dim3(kThreads), 0, s,
+                     reinterpret_cast<const unsigned long long*>(keys), (int)n_tokens, tab, budget);
+  return hipGetLastError();
+}
+
+hipError_t launch_l1_rel(const float* v, float* v_prev, long n_tokens, int channels, double* acc,
+                         bool first, hipStream_t s) {
+  if (n_tokens <= 0) return hipSuccess;
+  hipLaunchKernelGGL(l1_rel_accumulate, dim3(grid_for(n_tokens)), dim3(kThreads), 0, s, v, v_prev,
+                     n_tokens, channels, acc, first ? 1 : 0);
+  return hipGetLastError();
+}
+
 hipError_t launch_assign_budgets(const float* v, long n_tokens, int channels,
                                  const GroupTable& tab, double* keys, int32_t* budget,
                                  hipStream_t s) {
@@ -244,10 +293,7 @@ hipError_t launch_assign_budgets(const float* v, long n_tokens, int channels,
                        n_tokens, channels, keys);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const unsigned blocks = (unsigned)((n_tokens + kRankTokens - 1) / kRankTokens);
-  hipLaunchKernelGGL(rank_budgets, dim3(blocks), dim3(kThreads), 0, s,
-                     reinterpret_cast<const unsigned long long*>(keys), (int)n_tokens, tab, budget);
-  return hipGetLastError();
+  return launch_rank_budgets(keys, n_tokens, tab, budget, s);
 }
 
 }  // namespace hsa

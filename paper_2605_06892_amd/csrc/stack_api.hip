@@ -122,7 +122,7 @@ HSA_API int hsa_row_rms_scale(int dtype, const void* x, int32_t n_rows, int32_t 
 }
 
 HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, const void* w,
-                       int32_t d_out, const float* row_scale, const void* residual,
+                       int32_t d_out, const float* row_scale, const void* residual, int32_t gelu,
                        int out_dtype, void* y, hipStream_t stream) {
   const size_t es = elem_size(dtype), oes = elem_size(out_dtype);
   if (!es || !oes) return HSA_STEP_ERR_DTYPE;
@@ -130,7 +130,8 @@ HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, c
     return HSA_STEP_ERR_DTYPE;
   const bool f32_out = dtype == HSA_STEP_BF16 && out_dtype == HSA_STEP_F32;
   if (n_rows < 0 || d_in <= 0 || d_out <= 0) return HSA_STEP_ERR_SHAPE;
-  if (f32_out && residual) return HSA_STEP_ERR_SHAPE;
+  if ((f32_out || gelu) && residual) return HSA_STEP_ERR_SHAPE;
+  if (f32_out && gelu) return HSA_STEP_ERR_SHAPE;
   if (dtype == HSA_STEP_BF16 && (d_in % 64 != 0 || d_out % 4 != 0)) return HSA_STEP_ERR_SHAPE;
   if (n_rows == 0) return HSA_STEP_OK;
   if (!x || !w || !y) return HSA_STEP_ERR_NULL;
@@ -143,8 +144,9 @@ HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, c
       overlaps(y, yb, w, (size_t)d_out * d_in * es) || overlaps(y, yb, row_scale, (size_t)n_rows * 4))
     return HSA_STEP_ERR_ALIAS;
   if (residual && residual != y && overlaps(y, yb, residual, yb)) return HSA_STEP_ERR_ALIAS;
-  return launch_status(launch_gemm(
-      dtype, compact_gemm(x, n_rows, d_in, w, d_out, row_scale, residual, f32_out, y), stream));
+  RowGemm g = compact_gemm(x, n_rows, d_in, w, d_out, row_scale, residual, f32_out, y);
+  g.gelu = gelu ? 1 : 0;
+  return launch_status(launch_gemm(dtype, g, stream));
 }
 
 HSA_API size_t hsa_assign_budgets_workspace_bytes(int64_t n_tokens) {
@@ -172,24 +174,56 @@ HSA_API int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channel
                                                   static_cast<double*>(workspace), budget, stream));
 }
 
+HSA_API int hsa_l1_rel_accumulate(const float* v, float* v_prev, int64_t n_tokens,
+                                  int32_t channels, double* acc, int32_t first,
+                                  hipStream_t stream) {
+  if (n_tokens < 0 || n_tokens > kMaxRows || channels < 0) return HSA_STEP_ERR_SHAPE;
+  if (n_tokens == 0) return HSA_STEP_OK;
+  if (!v || !v_prev || !acc) return HSA_STEP_ERR_NULL;
+  if (!aligned(v, 4) || !aligned(v_prev, 4) || !aligned(acc, 8)) return HSA_STEP_ERR_SHAPE;
+  const size_t vb = (size_t)n_tokens * channels * 4, ab = (size_t)n_tokens * 8;
+  if (overlaps(v_prev, vb, v, vb) || overlaps(acc, ab, v, vb) || overlaps(acc, ab, v_prev, vb))
+    return HSA_STEP_ERR_ALIAS;
+  return launch_status(hsa::launch_l1_rel(v, v_prev, n_tokens, channels, acc, first != 0, stream));
+}
+
+HSA_API int hsa_assign_budgets_by_key(const double* keys, int64_t n_tokens, int32_t T,
+                                      const int32_t* group_budget, const int64_t* group_size,
+                                      int32_t n_groups, int32_t* budget, hipStream_t stream) {
+  if (n_tokens < 0 || n_tokens > kMaxRows) return HSA_STEP_ERR_SHAPE;
+  hsa::GroupTable tab{};
+  const int st = make_group_table(T, group_budget, group_size, n_groups, n_tokens, &tab);
+  if (st != HSA_STEP_OK) return st;
+  if (n_tokens == 0) return HSA_STEP_OK;
+  if (!keys || !budget) return HSA_STEP_ERR_NULL;
+  if (!aligned(keys, 8) || !aligned(budget, 4)) return HSA_STEP_ERR_SHAPE;
+  if (overlaps(budget, (size_t)n_tokens * 4, keys, (size_t)n_tokens * 8)) return HSA_STEP_ERR_ALIAS;
+  return launch_status(hsa::launch_rank_budgets(keys, n_tokens, tab, budget, stream));
+}
+
 HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int32_t margin,
                                 int32_t outside_period, float sigma_i, float sigma_next,
-                                const int32_t* group_budget,
-                                const int64_t* group_size, int32_t n_groups,
-                                int32_t* n_active_host, int32_t* refreshed_host,
-                                hipStream_t stream) {
+                                const int32_t* group_budget, const int64_t* group_size,
+                                int32_t n_groups, int32_t selection, int32_t* n_active_host,
+                                int32_t* refreshed_host, hipStream_t stream) {
   if (!s) return HSA_STEP_ERR_NULL;
   const size_t es = elem_size(s->dtype);
   if (!es) return HSA_STEP_ERR_DTYPE;
   const int64_t N = s->n_tokens;
   const int L = s->n_layers, C = s->channels, dh = s->head_dim;
+  const int F = s->ffn_dim, Lc = s->ctx_len;
   if (N < 1 || N > kMaxRows || L < 0 || s->heads <= 0 || (dh != 64 && dh != 128) || C <= 0 ||
-      s->reserved != 0 || (int64_t)s->heads * dh > INT32_MAX / 4)
+      s->reserved != 0 || (int64_t)s->heads * dh > INT32_MAX / 4 || F < 0 || Lc < 0 ||
+      Lc > kMaxRows)
     return HSA_STEP_ERR_SHAPE;
   const int d = s->heads * dh;
-  if (s->dtype == HSA_STEP_BF16 && C % 64 != 0) return HSA_STEP_ERR_SHAPE;
+  if (s->dtype == HSA_STEP_BF16 && (C % 64 != 0 || F % 64 != 0)) return HSA_STEP_ERR_SHAPE;
   if (T < 1 || iter < 0 || iter >= T || margin < 0 || margin > T / 2) return HSA_STEP_ERR_BUDGET;
   if (outside_period < 1 || T % outside_period != 0) return HSA_STEP_ERR_BUDGET;
+  if (selection != HSA_SELECT_VELOCITY_NORM && selection != HSA_SELECT_L1_REL)
+    return HSA_STEP_ERR_BUDGET;
+  const bool l1rel = n_groups != 0 && selection == HSA_SELECT_L1_REL;
+  if (l1rel && (margin < 2 || outside_period != 1)) return HSA_STEP_ERR_BUDGET;
   hsa::GroupTable tab{};
   if (n_groups != 0) {
     if (n_groups < 0) return HSA_STEP_ERR_BUDGET;
@@ -198,13 +232,14 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   }
   if (!s->w_embed || !s->w_head || !s->x || !s->v_hat || !s->budget || !s->idx || !s->n_active ||
       !s->xa || !s->h || !s->q || !s->o || !s->v_fresh || !s->row_scale ||
-      (n_groups && !s->keys))
+      (n_groups && !s->keys) || (l1rel && !s->v_prev) || (F > 0 && !s->f))
     return HSA_STEP_ERR_NULL;
-  if (L > 0 && (!s->w_layers || !s->caches)) return HSA_STEP_ERR_NULL;
+  if (L > 0 && (!s->w_layers || !s->caches || (Lc > 0 && !s->w_cross) || (F > 0 && !s->w_ffn)))
+    return HSA_STEP_ERR_NULL;
   for (int i = 0; i < 4 * L; ++i)
-    if (!s->w_layers[i]) return HSA_STEP_ERR_NULL;
+    if (!s->w_layers[i] || (Lc > 0 && !s->w_cross[i])) return HSA_STEP_ERR_NULL;
   for (int i = 0; i < 2 * L; ++i)
-    if (!s->caches[i]) return HSA_STEP_ERR_NULL;
+    if (!s->caches[i] || (F > 0 && !s->w_ffn[i])) return HSA_STEP_ERR_NULL;
 
   const size_t row_d = (size_t)d * es, row_c = (size_t)C * es;
   std::vector<Span> written = {
@@ -213,9 +248,19 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       {s->h, (size_t)N * row_d},   {s->q, (size_t)N * row_d},     {s->o, (size_t)N * row_d},
       {s->v_fresh, (size_t)N * C * 4}, {s->row_scale, (size_t)N * 4}};
   if (n_groups) written.push_back({s->keys, (size_t)N * 8});
+  if (l1rel) written.push_back({s->v_prev, (size_t)N * C * 4});
+  if (F > 0) written.push_back({s->f, (size_t)N * F * es});
   for (int i = 0; i < 2 * L; ++i) written.push_back({s->caches[i], (size_t)N * row_d});
   std::vector<Span> weights = {{s->w_embed, (size_t)d * row_c}, {s->w_head, (size_t)C * row_d}};
   for (int i = 0; i < 4 * L; ++i) weights.push_back({s->w_layers[i], (size_t)d * row_d});
+  for (int l = 0; l < L && Lc > 0; ++l) {
+    const void* const* wc = s->w_cross + 4 * l;
+    weights.push_back({wc[0], (size_t)d * row_d});
+    weights.push_back({wc[1], (size_t)d * row_d});
+    weights.push_back({wc[2], (size_t)Lc * row_d});
+    weights.push_back({wc[3], (size_t)Lc * row_d});
+  }
+  for (int i = 0; i < 2 * L && F > 0; ++i) weights.push_back({s->w_ffn[i], (size_t)F * row_d});
   for (const Span& b : written)
     if (!aligned(b.p, 16)) return HSA_STEP_ERR_SHAPE;
   for (const Span& b : weights)
@@ -238,18 +283,22 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   const int dt = s->dtype;
   const bool bf = dt == HSA_STEP_BF16;
   const float scale = 1.0f / sqrtf((float)dh);
+  auto ok = [](hipError_t e) { return e == hipSuccess; };
+  auto rms = [&]() { return ok(hsa::launch_row_rms_scale(s->h, bf, n, d, kRmsEps, s->row_scale, stream)); };
+  auto attend = [&](const void* q, const void* k, const void* v, int n_kv) {
+    return ok(bf ? hsa::launch_attention_bf16(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream)
+                 : hsa::launch_attention_f32(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream));
+  };
+  auto gemm = [&](const RowGemm& g) { return ok(launch_gemm(dt, g, stream)); };
   if (n > 0) {
-    if (hsa::launch_gather_latent(s->x, s->idx, n, N, C, bf, s->xa, stream) != hipSuccess)
-      return HSA_STEP_ERR_LAUNCH;
-    if (launch_gemm(dt, compact_gemm(s->xa, n, C, s->w_embed, d, nullptr, nullptr, false, s->h),
-                    stream) != hipSuccess)
+    if (!ok(hsa::launch_gather_latent(s->x, s->idx, n, N, C, bf, s->xa, stream)) ||
+        !gemm(compact_gemm(s->xa, n, C, s->w_embed, d, nullptr, nullptr, false, s->h)))
       return HSA_STEP_ERR_LAUNCH;
     for (int l = 0; l < L; ++l) {
       const void* const* w = s->w_layers + 4 * l;
       void* kc = s->caches[2 * l];
       void* vc = s->caches[2 * l + 1];
-      if (hsa::launch_row_rms_scale(s->h, bf, n, d, kRmsEps, s->row_scale, stream) != hipSuccess)
-        return HSA_STEP_ERR_LAUNCH;
+      // self-attention: Q/K/V of rms(h) with the cache overwrite, all N cached rows
       RowGemm g{};
       g.A = s->h;
       g.a_rows = nullptr;
@@ -263,35 +312,52 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       g.out[2] = {w[2], vc, s->idx, (int)N};
       g.n_out = 3;
       g.row_scale = s->row_scale;
-      if (launch_gemm(dt, g, stream) != hipSuccess) return HSA_STEP_ERR_LAUNCH;
-      const hipError_t e =
-          bf ? hsa::launch_attention_bf16(s->q, kc, vc, s->o, n, (int)N, s->heads, dh, scale, stream)
-             : hsa::launch_attention_f32(s->q, kc, vc, s->o, n, (int)N, s->heads, dh, scale, stream);
-      if (e != hipSuccess) return HSA_STEP_ERR_LAUNCH;
-      if (launch_gemm(dt, compact_gemm(s->o, n, d, w[3], d, nullptr, s->h, false, s->h), stream) !=
-          hipSuccess)
+      if (!rms() || !gemm(g) || !attend(s->q, kc, vc, (int)N) ||
+          !gemm(compact_gemm(s->o, n, d, w[3], d, nullptr, s->h, false, s->h)))
         return HSA_STEP_ERR_LAUNCH;
+      if (Lc > 0) {  // cross-attention of the active rows to the context
+        const void* const* wc = s->w_cross + 4 * l;
+        if (!rms() || !gemm(compact_gemm(s->h, n, d, wc[0], d, s->row_scale, nullptr, false, s->q)) ||
+            !attend(s->q, wc[2], wc[3], Lc) ||
+            !gemm(compact_gemm(s->o, n, d, wc[1], d, nullptr, s->h, false, s->h)))
+          return HSA_STEP_ERR_LAUNCH;
+      }
+      if (F > 0) {  // feed-forward network of the active rows
+        const void* const* wf = s->w_ffn + 2 * l;
+        RowGemm up = compact_gemm(s->h, n, d, wf[0], F, s->row_scale, nullptr, false, s->f);
+        up.gelu = 1;
+        if (!rms() || !gemm(up) ||
+            !gemm(compact_gemm(s->f, n, F, wf[1], d, nullptr, s->h, false, s->h)))
+          return HSA_STEP_ERR_LAUNCH;
+      }
     }
-    if (hsa::launch_row_rms_scale(s->h, bf, n, d, kRmsEps, s->row_scale, stream) != hipSuccess)
-      return HSA_STEP_ERR_LAUNCH;
-    if (launch_gemm(dt, compact_gemm(s->h, n, d, s->w_head, C, s->row_scale, nullptr, bf, s->v_fresh),
-                    stream) != hipSuccess)
+    if (!rms() ||
+        !gemm(compact_gemm(s->h, n, d, s->w_head, C, s->row_scale, nullptr, bf, s->v_fresh)))
       return HSA_STEP_ERR_LAUNCH;
   }
 
   // 3. velocity cache refresh of the active rows, Euler step of every token
   const float dsig = sigma_next - sigma_i;  // fp32 difference
-  if (hsa::launch_cached_euler(s->x, s->v_hat, n > 0 ? s->v_fresh : nullptr, s->idx, n, N, C, dsig,
-                               stream) != hipSuccess)
+  if (!ok(hsa::launch_cached_euler(s->x, s->v_hat, n > 0 ? s->v_fresh : nullptr, s->idx, n, N, C,
+                                   dsig, stream)))
     return HSA_STEP_ERR_LAUNCH;
 
-  // 4. group refresh where every group's schedule fires
-  if (n_groups && iter % refresh_period(T, group_budget, n_groups) == 0) {
+  // 4. group membership
+  double* keys = static_cast<double*>(s->keys);
+  if (n_groups && !l1rel && iter % refresh_period(T, group_budget, n_groups) == 0) {
     if (n != N) return HSA_STEP_ERR_BUDGET;
-    if (hsa::launch_assign_budgets(s->v_hat, N, C, tab, static_cast<double*>(s->keys), s->budget,
-                                   stream) != hipSuccess)
+    if (!ok(hsa::launch_assign_budgets(s->v_hat, N, C, tab, keys, s->budget, stream)))
       return HSA_STEP_ERR_LAUNCH;
     if (refreshed_host) *refreshed_host = 1;
+  }
+  if (l1rel && iter < margin) {
+    if (n != N) return HSA_STEP_ERR_BUDGET;
+    if (!ok(hsa::launch_l1_rel(s->v_hat, s->v_prev, N, C, keys, iter == 0, stream)))
+      return HSA_STEP_ERR_LAUNCH;
+    if (iter == margin - 1) {
+      if (!ok(hsa::launch_rank_budgets(keys, N, tab, s->budget, stream))) return HSA_STEP_ERR_LAUNCH;
+      if (refreshed_host) *refreshed_host = 1;
+    }
   }
   return HSA_STEP_OK;
 }

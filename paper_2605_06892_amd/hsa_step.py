@@ -61,11 +61,13 @@ def lib() -> ctypes.CDLL:
             "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
             "hsa_gather_rows": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P]),
             "hsa_row_rms_scale": (ctypes.c_int, [ctypes.c_int, P, I32, I32, F, P, P]),
-            "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, P, ctypes.c_int, P, P]),
+            "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, P, I32, ctypes.c_int, P, P]),
+            "hsa_l1_rel_accumulate": (ctypes.c_int, [P, P, I64, I32, P, I32, P]),
+            "hsa_assign_budgets_by_key": (ctypes.c_int, [P, I64, I32, P, P, I32, P, P]),
             "hsa_assign_budgets_workspace_bytes": (S, [I64]),
             "hsa_assign_budgets": (ctypes.c_int, [P, I64, I32, I32, P, P, I32, P, P, S, P]),
             "hsa_stack_iteration": (ctypes.c_int, [ctypes.POINTER(HsaStack), I32, I32, I32, I32, F, F, P, P,
-                                                   I32, P, P, P]),
+                                                   I32, I32, P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -90,8 +92,13 @@ EXPORTED = (
     "hsa_linear",
     "hsa_assign_budgets_workspace_bytes",
     "hsa_assign_budgets",
+    "hsa_l1_rel_accumulate",
+    "hsa_assign_budgets_by_key",
     "hsa_stack_iteration",
 )
+
+SELECT_VELOCITY_NORM = 0
+SELECT_L1_REL = 1
 
 
 class HsaStack(ctypes.Structure):
@@ -107,6 +114,9 @@ class HsaStack(ctypes.Structure):
         ("idx", ctypes.c_void_p), ("n_active", ctypes.c_void_p), ("xa", ctypes.c_void_p),
         ("h", ctypes.c_void_p), ("q", ctypes.c_void_p), ("o", ctypes.c_void_p),
         ("v_fresh", ctypes.c_void_p), ("keys", ctypes.c_void_p), ("row_scale", ctypes.c_void_p),
+        ("ffn_dim", ctypes.c_int32), ("ctx_len", ctypes.c_int32),
+        ("w_cross", ctypes.POINTER(ctypes.c_void_p)), ("w_ffn", ctypes.POINTER(ctypes.c_void_p)),
+        ("f", ctypes.c_void_p), ("v_prev", ctypes.c_void_p),
     ]
 
 
@@ -242,14 +252,14 @@ def hsa_row_rms_scale(x, n_rows: int, scale, eps: float = RMS_EPS, stream=None) 
     _check("hsa_row_rms_scale", st)
 
 
-def hsa_linear(x, n_rows: int, w, y, residual=None, row_scale=None, stream=None) -> None:
-    """y[:n_rows] = row_scale * (x[:n_rows] w^T) (+ residual[:n_rows]); y's
-    dtype is the output dtype (x's, or fp32 for bf16 x)."""
+def hsa_linear(x, n_rows: int, w, y, residual=None, row_scale=None, gelu: bool = False, stream=None) -> None:
+    """y[:n_rows] = act(row_scale * (x[:n_rows] w^T)) (+ residual[:n_rows]);
+    y's dtype is the output dtype (x's, or fp32 for bf16 x)."""
     _dev(x, w, y, residual, row_scale)
     dt = _dtype(x, w)
     d_out, d_in = w.shape
-    st = lib().hsa_linear(dt, _ptr(x), n_rows, d_in, _ptr(w), d_out, _ptr(row_scale), _ptr(residual), _dtype(y),
-                          _ptr(y), _stream(stream))
+    st = lib().hsa_linear(dt, _ptr(x), n_rows, d_in, _ptr(w), d_out, _ptr(row_scale), _ptr(residual), int(gelu),
+                          _dtype(y), _ptr(y), _stream(stream))
     _check("hsa_linear", st)
 
 
@@ -276,13 +286,32 @@ def hsa_assign_budgets(v, T: int, group_sizes, budget, workspace, stream=None) -
     _check("hsa_assign_budgets", st)
 
 
+def hsa_l1_rel_accumulate(v, v_prev, acc, first: bool, stream=None) -> None:
+    _dev(v, v_prev, acc)
+    n_tokens, channels = v.shape
+    st = lib().hsa_l1_rel_accumulate(_ptr(v), _ptr(v_prev), n_tokens, channels, _ptr(acc), int(first),
+                                     _stream(stream))
+    _check("hsa_l1_rel_accumulate", st)
+
+
+def hsa_assign_budgets_by_key(keys, T: int, group_sizes, budget, stream=None) -> None:
+    _dev(keys, budget)
+    gb, gs, n = _group_arrays(group_sizes)
+    st = lib().hsa_assign_budgets_by_key(_ptr(keys), keys.numel(), T, gb, gs, n, _ptr(budget), _stream(stream))
+    _check("hsa_assign_budgets_by_key", st)
+
+
 def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_active, xa, h, q, o, v_fresh,
-               keys, row_scale, heads: int, head_dim: int) -> HsaStack:
+               keys, row_scale, heads: int, head_dim: int, cross=None, ffn=None, f=None,
+               v_prev=None) -> HsaStack:
     """Fill a struct hsa_stack from device tensors. layers: per layer
-    (wq, wk, wv, wo); caches: per layer (k_hat, v_hat). The returned struct
-    keeps its host pointer arrays alive; the tensors must outlive it."""
-    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale]
+    (wq, wk, wv, wo); caches: per layer (k_hat, v_hat); cross: per layer
+    (wq_c, wo_c, k_c, v_c) or None; ffn: per layer (w1, w2) or None. The
+    returned struct keeps its host pointer arrays alive; the tensors must
+    outlive it."""
+    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale, f, v_prev]
     ts += [t for lw in layers for t in lw] + [t for c in caches for t in c]
+    ts += [t for lw in (cross or ()) for t in lw] + [t for lw in (ffn or ()) for t in lw]
     _dev(*ts)
     n_tokens, channels = x.shape
     wl = (ctypes.c_void_p * max(1, 4 * len(layers)))(*[t.data_ptr() for lw in layers for t in lw])
@@ -296,18 +325,30 @@ def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_acti
                  x=x.data_ptr(), v_hat=v_hat.data_ptr(), budget=budget.data_ptr(), idx=idx.data_ptr(),
                  n_active=n_active.data_ptr(), xa=xa.data_ptr(), h=h.data_ptr(), q=q.data_ptr(),
                  o=o.data_ptr(), v_fresh=v_fresh.data_ptr(), keys=keys.data_ptr(),
-                 row_scale=row_scale.data_ptr())
-    s._keep = (wl, cl)
+                 row_scale=row_scale.data_ptr(), ffn_dim=0 if not ffn else ffn[0][0].shape[0],
+                 ctx_len=0 if not cross else cross[0][2].shape[0],
+                 f=0 if f is None else f.data_ptr(), v_prev=0 if v_prev is None else v_prev.data_ptr())
+    keep = [wl, cl]
+    if cross:
+        xl = (ctypes.c_void_p * (4 * len(cross)))(*[t.data_ptr() for lw in cross for t in lw])
+        s.w_cross = ctypes.cast(xl, ctypes.POINTER(ctypes.c_void_p))
+        keep.append(xl)
+    if ffn:
+        fl = (ctypes.c_void_p * (2 * len(ffn)))(*[t.data_ptr() for lw in ffn for t in lw])
+        s.w_ffn = ctypes.cast(fl, ctypes.POINTER(ctypes.c_void_p))
+        keep.append(fl)
+    s._keep = tuple(keep)
     return s
 
 
 def hsa_stack_iteration(stack: HsaStack, T: int, iteration: int, margin: int, sigma_i: float,
-                        sigma_next: float, group_sizes=None, stream=None, outside_period: int = 1) -> tuple:
+                        sigma_next: float, group_sizes=None, stream=None, outside_period: int = 1,
+                        selection: int = SELECT_VELOCITY_NORM) -> tuple:
     """One multi-layer HSA iteration; returns (|A_i|, refreshed)."""
     gb, gs, n = _group_arrays(group_sizes or ())
     n_act = ctypes.c_int32(-1)
     ref = ctypes.c_int32(-1)
     st = lib().hsa_stack_iteration(ctypes.byref(stack), T, iteration, margin, outside_period, sigma_i, sigma_next,
-                                   gb, gs, n, ctypes.byref(n_act), ctypes.byref(ref), _stream(stream))
+                                   gb, gs, n, selection, ctypes.byref(n_act), ctypes.byref(ref), _stream(stream))
     _check("hsa_stack_iteration", st)
     return n_act.value, bool(ref.value)

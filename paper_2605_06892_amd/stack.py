@@ -36,8 +36,12 @@ class StackBuffers:
     v_fresh: torch.Tensor    # [N, C] fp32
     keys: torch.Tensor       # float64 [N]
     row_scale: torch.Tensor  # fp32 [N]
+    v_prev: torch.Tensor     # [N, C] fp32 (strategy D)
     heads: int
     head_dim: int
+    cross: list | None = None   # per layer (wq_c, wo_c, k_c, v_c); k_c, v_c [ctx, d]
+    ffn: list | None = None     # per layer (w1 [F, d], w2 [d, F])
+    f: torch.Tensor | None = None  # [N, F]
     _handle: H.HsaStack | None = field(default=None, repr=False)
 
     @property
@@ -54,7 +58,10 @@ class StackBuffers:
 
     @classmethod
     def allocate(cls, N: int, C: int, n_layers: int, heads: int, head_dim: int, dtype: torch.dtype,
-                 device="cuda") -> "StackBuffers":
+                 device="cuda", ffn: int = 0, ctx: int = 0) -> "StackBuffers":
+        """Tensors for N tokens, C latent values per token, n_layers layers of
+        width heads * head_dim; ffn > 0 / ctx > 0 add the FFN and
+        cross-attention sub-layers of full blocks."""
         d = heads * head_dim
         e = lambda *s, dt=dtype: torch.empty(*s, dtype=dt, device=device)  # noqa: E731
         f32 = torch.float32
@@ -64,7 +71,17 @@ class StackBuffers:
                    caches=[(e(N, d), e(N, d)) for _ in range(n_layers)],
                    idx=e(N, dt=torch.int32), n_active=e(1, dt=torch.int32), xa=e(N, C), h=e(N, d), q=e(N, d),
                    o=e(N, d), v_fresh=e(N, C, dt=f32), keys=e(N, dt=torch.float64), row_scale=e(N, dt=f32),
-                   heads=heads, head_dim=head_dim)
+                   v_prev=e(N, C, dt=f32), heads=heads, head_dim=head_dim,
+                   cross=[(e(d, d), e(d, d), e(ctx, d), e(ctx, d)) for _ in range(n_layers)] if ctx else None,
+                   ffn=[(e(ffn, d), e(d, ffn)) for _ in range(n_layers)] if ffn else None,
+                   f=e(N, ffn) if ffn else None)
+
+    def set_context(self, ctx: torch.Tensor, wk_c, wv_c) -> None:
+        """K_c = ctx Wk_c^T and V_c = ctx Wv_c^T of every layer, computed once
+        per sample on the device (hsa_linear)."""
+        for (_, _, kc, vc), wk, wv in zip(self.cross, wk_c, wv_c):
+            H.hsa_linear(ctx, ctx.shape[0], wk, kc)
+            H.hsa_linear(ctx, ctx.shape[0], wv, vc)
 
     def handle(self) -> H.HsaStack:
         """The struct hsa_stack describing these tensors (built once)."""
@@ -73,20 +90,23 @@ class StackBuffers:
                                         w_head=self.w_head, layers=self.layers, caches=self.caches, idx=self.idx,
                                         n_active=self.n_active, xa=self.xa, h=self.h, q=self.q, o=self.o,
                                         v_fresh=self.v_fresh, keys=self.keys, row_scale=self.row_scale,
-                                        heads=self.heads, head_dim=self.head_dim)
+                                        heads=self.heads, head_dim=self.head_dim, cross=self.cross,
+                                        ffn=self.ffn, f=self.f, v_prev=self.v_prev)
         return self._handle
 
 
 def iteration(b: StackBuffers, T: int, i: int, sigmas, group_sizes=None, margin: int = 0,
-              outside_period: int = 1, stream=None) -> tuple:
+              outside_period: int = 1, selection: int = H.SELECT_VELOCITY_NORM, stream=None) -> tuple:
     """Iteration i of the sampler; returns (|A_i|, refreshed)."""
     return H.hsa_stack_iteration(b.handle(), T, i, margin, float(sigmas[i]), float(sigmas[i + 1]), group_sizes,
-                                 stream, outside_period)
+                                 stream, outside_period, selection)
 
 
 def run(b: StackBuffers, T: int, sigmas, group_sizes=None, margin: int = 0, iterations=None,
-        start: int = 0, outside_period: int = 1, stream=None) -> list:
+        start: int = 0, outside_period: int = 1, selection: int = H.SELECT_VELOCITY_NORM,
+        stream=None) -> list:
     """Iterations start .. start+iterations-1 (default: the whole trajectory);
     returns the (|A_i|, refreshed) of each."""
     stop = T if iterations is None else start + iterations
-    return [iteration(b, T, i, sigmas, group_sizes, margin, outside_period, stream) for i in range(start, stop)]
+    return [iteration(b, T, i, sigmas, group_sizes, margin, outside_period, selection, stream)
+            for i in range(start, stop)]

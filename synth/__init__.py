@@ -19,5 +19,6 @@ from .workloads import (  # noqa: F401
     draw_stack_state,
     group_sizes,
     linear_sigmas,
+    random_budgets,
     to_bf16_values,
 )

@@ -186,7 +186,8 @@ def draw_block(wl: Workload, seed: int = 0, n_tokens: int | None = None) -> dict
     return {"x": x, "wq": wq, "wk": wk, "wv": wv, "wo": wo, "v_group": v_group}
 
 
-def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np.ndarray:
+def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered", frame_tokens: int = 0,
+                   seed: int | None = None) -> np.ndarray:
     """Per-token step budgets (int32[N]) for a budget partition.
 
     Group sizes: floor(N * fraction) for every budget except the largest, which
@@ -197,7 +198,13 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
     layout "contiguous": consecutive index ranges in ascending budget order,
     the largest budget last (the reordered sequence of Section 2.5).
     layout "random": a seeded random permutation of the tokens (strategy R of
-    Appendix B), seeded from the v_group values.
+    Appendix B), seeded from `seed`, or from the v_group values if None.
+    layout "uniform": strategy U of Appendix B, every group spread over the
+    whole sequence: tokens ordered by frac(n * golden ratio), a low-discrepancy
+    order, and cut into consecutive blocks.
+    layout "first_frame": strategy F of Appendix B: the first frame_tokens
+    tokens (the first latent frame in row-major patch order) go to the
+    largest budget, the rest are placed at random (seeded as "random").
     """
     N = v_group.shape[0]
     order_groups = group_sizes(N, groups)
@@ -206,9 +213,19 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
         rank = np.argsort(norms, kind="stable")
     elif layout == "contiguous":
         rank = np.arange(N)
-    elif layout == "random":
-        seed = int(np.frombuffer(np.ascontiguousarray(v_group[:1], np.float32).tobytes(), np.uint32)[0])
+    elif layout in ("random", "first_frame"):
+        if seed is None:
+            seed = int(np.frombuffer(np.ascontiguousarray(v_group[:1], np.float32).tobytes(), np.uint32)[0])
         rank = np.random.default_rng(seed).permutation(N)
+        if layout == "first_frame":
+            if not 0 <= frame_tokens <= order_groups[-1][1]:
+                raise ValueError("the first frame must fit in the largest-budget group")
+            # frame tokens last in the order, so they fall in the largest-budget block
+            rest = rank[rank >= frame_tokens]
+            rank = np.concatenate([rest, np.arange(frame_tokens)])
+    elif layout == "uniform":
+        golden = (math.sqrt(5.0) - 1.0) / 2.0
+        rank = np.argsort(np.mod(np.arange(N, dtype=np.float64) * golden, 1.0), kind="stable")
     else:
         raise ValueError(f"unknown layout {layout!r}")
     budget = np.empty(N, dtype=np.int32)
@@ -217,6 +234,11 @@ def assign_budgets(v_group: np.ndarray, groups, layout: str = "scattered") -> np
         budget[rank[start:start + n]] = s
         start += n
     return budget
+
+
+def random_budgets(N: int, groups, seed: int) -> np.ndarray:
+    """Strategy R for N tokens: a seeded random permutation cut into groups."""
+    return assign_budgets(np.zeros((N, 1), np.float32), groups, "random", seed=seed)
 
 
 def group_sizes(N: int, groups) -> tuple:

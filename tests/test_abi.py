@@ -181,7 +181,7 @@ def test_gather_rows_errors(lib):
 
 
 def test_linear_errors(lib):
-    f = lambda *a: lib.hsa_linear(*a[:6], a[6] if len(a) > 10 else None, *a[-4:])  # noqa: E731
+    f = lambda *a: lib.hsa_linear(*a[:6], None, a[6], 0, *a[-3:])  # noqa: E731
     assert f(F32, A, 10, 64, B, 64, None, BF16, C, None) == DTYPE   # fp32 in, bf16 out
     assert f(9, A, 10, 64, B, 64, None, BF16, C, None) == DTYPE
     assert f(BF16, A, 10, 100, B, 64, None, BF16, C, None) == SHAPE  # bf16 d_in % 64
@@ -195,8 +195,10 @@ def test_linear_errors(lib):
     assert f(BF16, A, 10, 64, B, 64, None, BF16, C + 8, None) == SHAPE    # misaligned
     assert f(BF16, None, 0, 64, None, 64, None, BF16, None, None) == OK
     g = lib.hsa_linear
-    assert g(BF16, A, 10, 64, B, 64, C + 8, None, BF16, C, None) == ALIAS  # row scales inside y
-    assert g(BF16, A, 10, 64, B, 64, D + 2, None, BF16, C, None) == SHAPE  # misaligned row scales
+    assert g(BF16, A, 10, 64, B, 64, C + 8, None, 0, BF16, C, None) == ALIAS  # row scales inside y
+    assert g(BF16, A, 10, 64, B, 64, D + 2, None, 0, BF16, C, None) == SHAPE  # misaligned row scales
+    assert g(BF16, A, 10, 64, B, 64, None, D, 1, BF16, C, None) == SHAPE     # GELU takes no residual
+    assert g(BF16, A, 10, 64, B, 64, None, None, 1, F32, C, None) == SHAPE   # nor an fp32 output
 
 
 def test_row_rms_scale_errors(lib):
@@ -237,7 +239,7 @@ def _stack(**over):
     step = 1 << 32
     ptrs = {n: base + k * step for k, n in enumerate(
         ["w_embed", "w_head", "x", "v_hat", "budget", "idx", "n_active", "xa", "h", "q", "o", "v_fresh", "keys",
-         "row_scale"])}
+         "row_scale", "v_prev"])}
     L = over.pop("L", 2)
     wl = (ctypes.c_void_p * (4 * L))(*[0x7D0000000000 + k * step for k in range(4 * L)])
     cl = (ctypes.c_void_p * (2 * L))(*[0x7C0000000000 + k * step for k in range(2 * L)])
@@ -254,9 +256,9 @@ def test_stack_iteration_errors(lib):
     f = lib.hsa_stack_iteration
     gb = (ctypes.c_int32 * 2)(20, 40)
     gs = (ctypes.c_int64 * 2)(500, 500)
-    call = lambda s, T=40, i=1, m=0, g=2, b=gb, p=1: f(ctypes.byref(s), T, i, m, p, 1.0, 0.975, b, gs,  # noqa: E731
-                                                       g, None, None, None)
-    assert f(None, 40, 0, 0, 1, 1.0, 0.975, None, None, 0, None, None, None) == NULL
+    call = lambda s, T=40, i=1, m=0, g=2, b=gb, p=1, sel=0: f(ctypes.byref(s), T, i, m, p, 1.0, 0.975, b,  # noqa: E731
+                                                              gs, g, sel, None, None, None)
+    assert f(None, 40, 0, 0, 1, 1.0, 0.975, None, None, 0, 0, None, None, None) == NULL
     assert call(_stack(dtype=4)[0]) == DTYPE
     assert call(_stack(head_dim=96)[0]) == SHAPE
     assert call(_stack(channels=16)[0]) == SHAPE           # bf16 stacks need C % 64 == 0
@@ -267,6 +269,14 @@ def test_stack_iteration_errors(lib):
     assert call(_stack()[0], m=21) == BUDGET
     assert call(_stack()[0], p=3) == BUDGET                           # outside period must divide T
     assert call(_stack()[0], p=0) == BUDGET
+    assert call(_stack()[0], sel=2) == BUDGET                         # unknown selection
+    assert call(_stack()[0], sel=1, m=1) == BUDGET                    # strategy D needs margin >= 2
+    assert call(_stack()[0], sel=1, m=4, p=2) == BUDGET               # ... and every token active outside
+    assert call(_stack(v_prev=None)[0], sel=1, m=4) == NULL
+    assert call(_stack(ffn_dim=100)[0]) == SHAPE                      # bf16 FFN width % 64
+    assert call(_stack(ffn_dim=128)[0]) == NULL                       # FFN weights and scratch missing
+    assert call(_stack(ctx_len=-1)[0]) == SHAPE
+    assert call(_stack(ctx_len=77)[0]) == NULL                        # cross-attention weights missing
     assert call(_stack()[0], b=(ctypes.c_int32 * 2)(20, 30)) == BUDGET   # 30 does not divide 40
     assert call(_stack()[0], g=-1) == BUDGET
     assert call(_stack(h=None)[0]) == NULL
@@ -283,3 +293,21 @@ def test_stack_iteration_errors(lib):
     assert call(s) == ALIAS                                            # a weight inside a cache
     assert call(_stack(q=0x7E0000000000 + 8 * (1 << 32) + 32)[0]) == ALIAS  # q inside h
     assert call(_stack(o=0x7E0000000000 + 3)[0]) == SHAPE              # misaligned
+
+
+def test_l1_rel_and_key_assignment_errors(lib):
+    f = lib.hsa_l1_rel_accumulate
+    assert f(A, B, -1, 16, C, 1, None) == SHAPE
+    assert f(None, B, 100, 16, C, 1, None) == NULL
+    assert f(A, A + 64, 100, 16, C, 0, None) == ALIAS      # v_prev inside v
+    assert f(A, B, 100, 16, B + 8, 0, None) == ALIAS       # acc inside v_prev
+    assert f(A, B, 100, 16, C + 4, 0, None) == SHAPE       # misaligned acc
+    assert f(None, None, 0, 16, None, 0, None) == OK
+    g = lib.hsa_assign_budgets_by_key
+    gb = (ctypes.c_int32 * 2)(10, 40)
+    gs = (ctypes.c_int64 * 2)(50, 50)
+    assert g(A, 100, 40, (ctypes.c_int32 * 2)(40, 10), gs, 2, B, None) == BUDGET
+    assert g(A, 100, 40, gb, (ctypes.c_int64 * 2)(50, 40), 2, B, None) == BUDGET
+    assert g(None, 100, 40, gb, gs, 2, B, None) == NULL
+    assert g(A, 100, 40, gb, gs, 2, A + 16, None) == ALIAS
+    assert g(A + 4, 100, 40, gb, gs, 2, B, None) == SHAPE

@@ -75,6 +75,9 @@ def test_row_rms_scale(dtype, n, d):
     ("f32", 301, 128, 128, "residual"),
     ("f32", 300, 128, 16, "plain"),
     ("f32", 300, 128, 48, "normed"),
+    ("bf16", 500, 256, 512, "normed_gelu"),  # FFN up-projection of rms(h)
+    ("bf16", 64, 1536, 8960, "normed_gelu"),
+    ("f32", 300, 128, 256, "normed_gelu"),
 ])
 def test_linear(dtype, n, d_in, d_out, mode):
     rng = np.random.default_rng(n + d_in + d_out)
@@ -92,8 +95,12 @@ def test_linear(dtype, n, d_in, d_out, mode):
         s = torch.empty(n, device=DEV)
         H.hsa_row_rms_scale(xd, n, s)
         y = torch.zeros((n, d_out), dtype=torch_dtype(out_dt), device=DEV)
-        H.hsa_linear(xd, n, to_dev(w, dtype), y, row_scale=s)
-        want = oracle.linear(oracle.rms_normalize(x), w, out_dt)
+        gelu = mode.endswith("gelu")
+        H.hsa_linear(xd, n, to_dev(w, dtype), y, row_scale=s, gelu=gelu)
+        if gelu:
+            want = oracle.round_to(oracle.gelu_tanh(oracle.rms_normalize(x) @ w.astype(np.float64).T), out_dt)
+        else:
+            want = oracle.linear(oracle.rms_normalize(x), w, out_dt)
     else:
         y = torch.zeros((n, d_out), dtype=torch_dtype(out_dt), device=DEV)
         H.hsa_linear(to_dev(x, dtype), n, to_dev(w, dtype), y)
@@ -132,6 +139,28 @@ def test_assign_budgets(N, C, case):
                                            oracle.velocity_keys(v)).view(np.uint64))
 
 
+def test_l1_rel_accumulate_and_assign_by_key():
+    rng = np.random.default_rng(77)
+    N, C = 5000, 64
+    vs = [rng.standard_normal((N, C)).astype(np.float32) for _ in range(3)]
+    vs[1][7] = 0.0                      # x / 0 -> inf
+    vs[1][8] = vs[0][8] = 0.0           # 0 / 0 -> NaN
+    acc = torch.full((N,), 5.0, dtype=torch.float64, device=DEV)
+    v_prev = torch.zeros((N, C), device=DEV)
+    for i, v in enumerate(vs):
+        H.hsa_l1_rel_accumulate(to_dev(v, "f32"), v_prev, acc, first=(i == 0))
+    want = oracle.l1_rel(vs[1], vs[0]) + oracle.l1_rel(vs[2], vs[1])
+    got = acc.cpu().numpy()
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(want))
+    fin = ~np.isnan(want)
+    np.testing.assert_array_equal(got[fin].view(np.uint64), want[fin].view(np.uint64))  # bit for bit
+    np.testing.assert_array_equal(host(v_prev), vs[2])
+    sizes = synth.group_sizes(N, ((40, .25), (20, .25), (10, .25), (5, .25)))
+    budget = torch.zeros(N, dtype=torch.int32, device=DEV)
+    H.hsa_assign_budgets_by_key(acc, 40, sizes, budget)
+    np.testing.assert_array_equal(budget.cpu().numpy(), oracle.assign_by_key(want, sizes))
+
+
 def test_assign_budgets_rejects_bad_groups():
     v = torch.zeros((8, 4), device=DEV)
     b = torch.zeros(8, dtype=torch.int32, device=DEV)
@@ -151,12 +180,23 @@ def test_assign_budgets_rejects_bad_groups():
 
 
 def _upload(wl, wts, N, L, state=None):
-    b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch_dtype(wl.dtype))
+    b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch_dtype(wl.dtype),
+                                ffn=wl.ffn, ctx=wl.ctx)
     b.w_embed.copy_(to_dev(wts["w_embed"], wl.dtype))
     b.w_head.copy_(to_dev(wts["w_head"], wl.dtype))
     for dst, lw in zip(b.layers, wts["layers"]):
         for t, k in zip(dst, ("wq", "wk", "wv", "wo")):
             t.copy_(to_dev(lw[k], wl.dtype))
+    if wl.ctx:
+        for dst, lw in zip(b.cross, wts["layers"]):
+            dst[0].copy_(to_dev(lw["wq_c"], wl.dtype))
+            dst[1].copy_(to_dev(lw["wo_c"], wl.dtype))
+        b.set_context(to_dev(wts["ctx"], wl.dtype), [to_dev(lw["wk_c"], wl.dtype) for lw in wts["layers"]],
+                      [to_dev(lw["wv_c"], wl.dtype) for lw in wts["layers"]])
+    if wl.ffn:
+        for dst, lw in zip(b.ffn, wts["layers"]):
+            dst[0].copy_(to_dev(lw["w1"], wl.dtype))
+            dst[1].copy_(to_dev(lw["w2"], wl.dtype))
     if state is None:
         b.x.copy_(to_dev(wts["x0"], "f32"))
         b.v_hat.zero_()
@@ -174,16 +214,20 @@ def _upload(wl, wts, N, L, state=None):
     return b
 
 
-def test_tiny_f32_stack_trajectory():
-    wl = synth.WORKLOADS["tiny_stack_f32"]
+@pytest.mark.parametrize("name,margin,selection", [("tiny_stack_f32", 0, "norm"), ("tiny_block_f32", 0, "norm"),
+                                                    ("tiny_stack_f32", 2, "l1rel"), ("tiny_block_f32", 3, "l1rel")])
+def test_tiny_f32_stack_trajectory(name, margin, selection):
+    wl = synth.WORKLOADS[name]
     wts = synth.draw_stack(wl, seed=0)
     sizes = synth.group_sizes(wl.N, wl.groups)
     sig = synth.linear_sigmas(wl.T)
-    recs = oracle.stack_trajectory(wts["x0"], wts, wl.T, sig, wl.heads, wl.dh, "f32", group_sizes=sizes)
+    recs = oracle.stack_trajectory(wts["x0"], wts, wl.T, sig, wl.heads, wl.dh, "f32", group_sizes=sizes,
+                                   margin=margin, selection=selection)
+    sel = H.SELECT_L1_REL if selection == "l1rel" else H.SELECT_VELOCITY_NORM
     b = _upload(wl, wts, wl.N, wl.layers)
     for r in recs:
-        keys = oracle.velocity_keys(r["v_hat"])
-        n, refreshed = S.iteration(b, wl.T, r["i"], sig, sizes)
+        keys = r["l1"] if selection == "l1rel" else oracle.velocity_keys(r["v_hat"])
+        n, refreshed = S.iteration(b, wl.T, r["i"], sig, sizes, margin=margin, selection=sel)
         assert (n, refreshed) == (r["idx"].size, r["refreshed"])
         np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), r["idx"])
         if refreshed:  # the ranking decisions are far from ties for this seed
@@ -204,9 +248,10 @@ def _state_for(wl, seed, N, L):
     return st
 
 
+@pytest.mark.parametrize("name", ["small_stack_bf16", "small_block_bf16"])
 @pytest.mark.parametrize("iteration", [1, 2, 0])  # 25% active, 50% active, all active + refresh
-def test_small_bf16_stack_iteration(iteration):
-    wl = synth.WORKLOADS["small_stack_bf16"]
+def test_small_bf16_stack_iteration(iteration, name):
+    wl = synth.WORKLOADS[name]
     N, L = wl.N, wl.layers
     wts = synth.draw_stack(wl, seed=31)
     st = _state_for(wl, 32, N, L)
@@ -297,3 +342,35 @@ def test_wan13b_stack_iterations():
     assert torch.equal(b.v_hat[act], b.v_fresh[:n])
     assert torch.isfinite(b.v_fresh[:n]).all()
     np.testing.assert_array_equal(b.budget.cpu().numpy(), budget1)
+
+
+def test_wan13b_full_blocks_iterations():
+    """Two full blocks (self-attention, cross-attention to a 512-row context,
+    FFN 8960) at the Wan-1.3B shape, all-active then 25%-active: skipped rows
+    of both layers' caches untouched, sampled layer-0 cache rows against the
+    oracle, fresh velocities finite, budgets from the velocity ranking."""
+    wl = synth.WORKLOADS["wan1.3b_blocks"]
+    N, L = wl.N, 2
+    wts = synth.draw_stack(wl, seed=1, layers=L)
+    sizes = synth.group_sizes(N, wl.groups)
+    sig = synth.linear_sigmas(wl.T)
+    b = _upload(wl, wts, N, L)
+    n, refreshed = S.iteration(b, wl.T, 0, sig, sizes)
+    assert (n, refreshed) == (N, True)
+    v0 = b.v_hat.cpu().numpy()
+    assert np.all(np.isfinite(v0))
+    budget1 = b.budget.cpu().numpy()
+    np.testing.assert_array_equal(budget1, oracle.assign_groups(v0, sizes))
+    rows = np.sort(np.random.default_rng(6).choice(N, 128, replace=False))
+    h0 = oracle.rms_normalize(oracle.linear(oracle.gather_latent(wts["x0"], rows, "bf16"), wts["w_embed"], "bf16"))
+    assert rel_inf(host(b.caches[0][0][rows]), oracle.linear(h0, wts["layers"][0]["wk"], "bf16")) <= TOL["bf16"]
+    assert rel_inf(host(b.caches[0][1][rows]), oracle.linear(h0, wts["layers"][0]["wv"], "bf16")) <= TOL["bf16"]
+    before = [(k.clone(), v.clone()) for k, v in b.caches]
+    n, refreshed = S.iteration(b, wl.T, 1, sig, sizes)
+    idx = oracle.active_set(budget1, wl.T, 1)
+    assert (n, refreshed) == (idx.size, False)
+    np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), idx)
+    skipped = torch.from_numpy(np.setdiff1d(np.arange(N), idx)).to(DEV)
+    for (k, v), (k0, v0_) in zip(b.caches, before):
+        assert torch.equal(k[skipped], k0[skipped]) and torch.equal(v[skipped], v0_[skipped])
+    assert torch.isfinite(b.v_fresh[:n]).all()
