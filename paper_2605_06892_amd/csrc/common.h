@@ -30,10 +30,14 @@ __device__ __forceinline__ int xcd_contiguous(int L, int total) {
 // Round fp32 to bf16, nearest-even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ bf16x4 to_bf16x4(f32x4 v) { return __builtin_convertvector(v, bf16x4); }
 
-// 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))
+// 0.5 x (1 + tanh(y)), y = sqrt(2/pi) (x + 0.044715 x^3), evaluated as
+// x / (1 + exp(-2y)) (the same function: 0.5 (1 + tanh(y)) is the logistic
+// function of 2y), with the hardware exp2 and reciprocal.
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  return 0.5f * x * (1.f + tanhf(k0 * fmaf(0.044715f * x, x * x, x)));
+  const float y = k0 * fmaf(0.044715f * x, x * x, x);
+  const float t = __builtin_amdgcn_exp2f(-2.8853900817779268f * y);  // exp(-2y)
+  return x * __builtin_amdgcn_rcpf(1.f + t);
 }
 
 __device__ __forceinline__ float wave_max(float v) {

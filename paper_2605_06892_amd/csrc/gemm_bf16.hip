@@ -226,11 +226,18 @@ hipError_t launch(const RowGemm& g, hipStream_t s) {
 
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.Nc <= 0 || (g.n_out != 1 && g.n_out != 3)) return hipSuccess;
-  // 256 x 256 tiles (8 waves of 128 x 64) for the three-output projection;
-  // 256 x 128 tiles (8 waves of 64 x 64) for the single-output one, whose grid
-  // would otherwise leave CUs idle in the last round of workgroups.
+  // 256 x 256 tiles (8 waves of 128 x 64) for the three-output projection and
+  // for single-output products with at least two workgroups per CU of them;
+  // 256 x 128 tiles (8 waves of 64 x 64) for smaller single-output products,
+  // whose grid would otherwise leave CUs idle in the last round.
   if (g.n_out == 3) return launch<256, 256, 2, 3, kEpiBf16>(g, s);
+  const long big = (long)((g.M + 255) / 256) * ((g.Nc + 255) / 256);
   if (g.c_f32) return launch<256, 128, 4, 1, kEpiF32>(g, s);
+  if (big >= 512) {
+    if (g.gelu) return launch<256, 256, 2, 1, kEpiBf16Gelu>(g, s);
+    if (g.residual) return launch<256, 256, 2, 1, kEpiBf16Residual>(g, s);
+    return launch<256, 256, 2, 1, kEpiBf16>(g, s);
+  }
   if (g.gelu) return launch<256, 128, 4, 1, kEpiBf16Gelu>(g, s);
   if (g.residual) return launch<256, 128, 4, 1, kEpiBf16Residual>(g, s);
   return launch<256, 128, 4, 1, kEpiBf16>(g, s);
