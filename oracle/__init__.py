@@ -25,6 +25,8 @@ from .hsa_oracle import (  # noqa: F401
 from .stack_oracle import (  # noqa: F401
     SELECT_L1REL,
     SELECT_NORM,
+    ROPE_THETA,
+    apply_rope,
     assign_by_key,
     assign_groups,
     boundary_gaps,
@@ -35,7 +37,10 @@ from .stack_oracle import (  # noqa: F401
     l1_rel,
     linear,
     refresh_period,
+    reorder_plan,
     rms_normalize,
+    rope_angles,
+    rope_bands,
     RMS_EPS,
     stack_forward,
     stack_iteration,

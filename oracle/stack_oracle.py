@@ -45,6 +45,16 @@ Readings where the paper is silent:
     latent channels times a 1x2x2 patch = 64) to d, no bias; the fp32
     latent rows are rounded once to the model dtype first. Velocity head: a
     linear map d -> C with an fp32 output. No timestep conditioning.
+  * RoPE subsampling (Section 2.3: the positional frequencies are subsampled
+    to the active set): with rotary embeddings on, Q and K of the active
+    rows are rotated by the positions of their own tokens in the latent
+    grid, never by their place in the compact active sequence. The paper
+    does not spell out the embedding; the reading is 3D rotary embedding
+    over (frame, row, column): the head dimension is cut into a temporal
+    band of dh - 4 floor(dh/6) channels and two spatial bands of
+    2 floor(dh/6) channels each; inside a band of b channels, the pair
+    (2j, 2j+1) at coordinate c turns by the angle c * theta^(-2j/b)
+    (theta = 10000). V is not rotated, nor is cross-attention.
   * Strategy D (Appendix B, Eq. 7) is taken as: over the initial full-budget
     steps -- the iterations 0 .. m-1 before the caching window, where every
     token is active -- the per-token L1_rel between consecutive fresh
@@ -68,7 +78,7 @@ import math
 
 import numpy as np
 
-from .hsa_oracle import active_set, attention, cached_euler, qkv_cache_update, round_to
+from .hsa_oracle import active_set, attention, cached_euler, check_budgets, qkv_cache_update, round_to
 
 
 # ---------------------------------------------------------------------------
@@ -82,6 +92,38 @@ def gather_latent(x, idx, dtype: str) -> np.ndarray:
 
 
 RMS_EPS = 1e-6
+
+
+ROPE_THETA = 10000.0
+
+
+def rope_bands(dh: int) -> tuple:
+    """Channel pairs of the temporal, row and column bands of one head."""
+    sp = dh // 6
+    return ((dh - 4 * sp) // 2, sp, sp)
+
+
+def rope_angles(positions, grid, dh: int, theta: float = ROPE_THETA) -> np.ndarray:
+    """Rotation angle of every channel pair of a head for tokens at the given
+    linear grid positions (frame-major, then row, then column): [M, dh/2]."""
+    F, H, W = grid
+    p = np.asarray(positions, np.int64)
+    coords = (p // (H * W), (p // W) % H, p % W)
+    cols = []
+    for n_pairs, c in zip(rope_bands(dh), coords):
+        j = np.arange(n_pairs, dtype=np.float64)
+        cols.append(c[:, None].astype(np.float64) * theta ** (-2.0 * j / (2 * n_pairs)))
+    return np.concatenate(cols, axis=1)
+
+
+def apply_rope(x, angles, heads: int, dh: int) -> np.ndarray:
+    """Rotate the channel pairs (2k, 2k+1) of every head of the rows of x by
+    angles[:, k], float64, unrounded."""
+    x = np.asarray(x, np.float64).reshape(x.shape[0], heads, dh // 2, 2)
+    c = np.cos(angles)[:, None, :]
+    s = np.sin(angles)[:, None, :]
+    a, b = x[..., 0], x[..., 1]
+    return np.stack([a * c - b * s, a * s + b * c], axis=-1).reshape(x.shape[0], heads * dh)
 
 
 def gelu_tanh(x) -> np.ndarray:
@@ -194,6 +236,18 @@ def boundary_gaps(keys, group_sizes) -> np.ndarray:
     return np.array(gaps)
 
 
+def reorder_plan(budget, T: int) -> tuple:
+    """Token reordering (Section 2.5): every non-baseline token (budget < T)
+    first, then the baseline group (budget T), each part in its old order.
+    Returns (perm, n_cached): new position i holds old token perm[i], and only
+    the first n_cached positions need cache rows (the baseline group is
+    active at every iteration, so its keys and values are always fresh)."""
+    b = check_budgets(budget, T)
+    lead = np.flatnonzero(b < T)
+    perm = np.concatenate([lead, np.flatnonzero(b == T)]).astype(np.int64)
+    return perm, int(lead.size)
+
+
 def refresh_period(T: int, budgets) -> int:
     """P = lcm of T/s_k: every group's schedule fires at the multiples of P."""
     p = 1
@@ -207,7 +261,7 @@ def refresh_period(T: int, budgets) -> int:
 # ---------------------------------------------------------------------------
 
 
-def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: str) -> dict:
+def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: str, rope=None) -> dict:
     """Embedding, L pre-norm layers (self-attention, and for full blocks
     cross-attention and FFN), final norm and velocity head for the active
     rows.
@@ -216,15 +270,31 @@ def stack_forward(xa, idx, weights: dict, caches, heads: int, dh: int, dtype: st
     (K_hat, V_hat) pair of [N, d] arrays per layer. Returns the fp32-valued
     fresh velocities [|A|, C], new copies of the caches (rows outside idx
     untouched) and the compact hidden state entering each layer and leaving
-    the last one.
+    the last one. rope: None, or {"grid": (F, H, W), "pos": original grid
+    position of every token (None: the token index), "theta": ...}; Q and K
+    of the active rows are then rotated by the positions of their tokens.
     """
     scale = 1.0 / math.sqrt(dh)
+    idx = np.asarray(idx, np.int64)
+    angles = None
+    if rope is not None:
+        pos = idx if rope.get("pos") is None else np.asarray(rope["pos"], np.int64)[idx]
+        angles = rope_angles(pos, rope["grid"], dh, rope.get("theta", ROPE_THETA))
     h = linear(xa, weights["w_embed"], dtype)
     hidden = [h]
     new_caches = []
     for lw, (k_hat, v_hat) in zip(weights["layers"], caches):
-        r = qkv_cache_update(rms_normalize(h), idx, lw["wq"], lw["wk"], lw["wv"], k_hat, v_hat, dtype,
-                             x_compact=True)
+        hn = rms_normalize(h)
+        if angles is None:
+            r = qkv_cache_update(hn, idx, lw["wq"], lw["wk"], lw["wv"], k_hat, v_hat, dtype, x_compact=True)
+        else:
+            prod = lambda w: hn @ np.asarray(w, np.float64).T  # noqa: E731
+            k = round_to(apply_rope(prod(lw["wk"]), angles, heads, dh), dtype)
+            r = {"q": round_to(apply_rope(prod(lw["wq"]), angles, heads, dh), dtype),
+                 "k_cache": np.array(k_hat, dtype=np.float64, copy=True),
+                 "v_cache": np.array(v_hat, dtype=np.float64, copy=True)}
+            r["k_cache"][idx] = k
+            r["v_cache"][idx] = round_to(prod(lw["wv"]), dtype)
         o = round_to(attention(r["q"], r["k_cache"], r["v_cache"], heads, dh, scale), dtype)
         h = linear(o, lw["wo"], dtype, residual=h)
         if "wq_c" in lw:  # cross-attention of the active rows to the fixed context
@@ -254,8 +324,9 @@ def initial_state(x0, n_layers: int, d: int, T: int) -> dict:
 
 def stack_iteration(state: dict, weights: dict, i: int, T: int, sigmas, heads: int, dh: int,
                     dtype: str, group_sizes=None, margin: int = 0, outside_period: int = 1,
-                    selection: str = SELECT_NORM) -> dict:
-    """One iteration of the multi-layer HSA sampler.
+                    selection: str = SELECT_NORM, rope=None) -> dict:
+    """One iteration of the multi-layer HSA sampler (rope as for
+    stack_forward).
 
     A_i from the budgets in force (and the window); the stack on the active
     rows (embedding of the gathered latent, each layer's cache overwrite and
@@ -278,7 +349,7 @@ def stack_iteration(state: dict, weights: dict, i: int, T: int, sigmas, heads: i
     N = x.shape[0]
     idx = active_set(state["budget"], T, i, margin, outside_period)
     xa = gather_latent(x, idx, dtype)
-    f = stack_forward(xa, idx, weights, state["caches"], heads, dh, dtype)
+    f = stack_forward(xa, idx, weights, state["caches"], heads, dh, dtype, rope)
     x_new, v_hat = cached_euler(x, state["v_hat"], f["v_fresh"], idx, sigmas[i], sigmas[i + 1])
     budget = state["budget"]
     v_prev, l1 = state.get("v_prev"), state.get("l1")
@@ -309,7 +380,7 @@ def stack_iteration(state: dict, weights: dict, i: int, T: int, sigmas, heads: i
 
 def stack_trajectory(x0, weights: dict, T: int, sigmas, heads: int, dh: int, dtype: str,
                      group_sizes=None, margin: int = 0, iterations=None, state=None,
-                     outside_period: int = 1, selection: str = SELECT_NORM) -> list:
+                     outside_period: int = 1, selection: str = SELECT_NORM, rope=None) -> list:
     """Iterations 0..T-1 (or the first `iterations`) of the multi-layer
     sampler from initial_state (or the given state). With group_sizes None
     and every budget T this is the dense flow-matching loop. Returns one
@@ -320,7 +391,7 @@ def stack_trajectory(x0, weights: dict, T: int, sigmas, heads: int, dh: int, dty
     records = []
     for i in range(T if iterations is None else iterations):
         r = stack_iteration(state, weights, i, T, sigmas, heads, dh, dtype, group_sizes, margin,
-                            outside_period, selection)
+                            outside_period, selection, rope)
         records.append(r)
         state = {"x": r["x"], "v_hat": r["v_hat"], "budget": r["budget"], "caches": r["caches"],
                  "v_prev": r["v_prev"], "l1": r["l1"]}

@@ -130,7 +130,7 @@ def test_refresh_period_is_where_every_group_fires(T, budgets):
 # ---------------------------------------------------------------------------
 
 
-def _torch_iteration(x, v_hat, caches, wts, idx, heads, dh, dsig, dtype="f32"):
+def _torch_iteration(x, v_hat, caches, wts, idx, heads, dh, dsig, dtype="f32", rotate=None):
     """Stack iteration written with torch's float64 linear, RMS norm and
     scaled-dot-product attention; each stored value is rounded to the model
     dtype (bf16 rounding by the separately pinned round_bf16), the velocity
@@ -144,9 +144,10 @@ def _torch_iteration(x, v_hat, caches, wts, idx, heads, dh, dsig, dtype="f32"):
     new_caches = []
     for lw, (kc, vc) in zip(wts["layers"], caches):
         hn = norm(h)
-        q = rnd(F.linear(hn, D(lw["wq"])))
+        rot = rotate or (lambda t: t)
+        q = rnd(rot(F.linear(hn, D(lw["wq"]))))
         K, V = D(kc).clone(), D(vc).clone()
-        K[ti] = rnd(F.linear(hn, D(lw["wk"])))
+        K[ti] = rnd(rot(F.linear(hn, D(lw["wk"]))))
         V[ti] = rnd(F.linear(hn, D(lw["wv"])))
         split = lambda t: t.view(t.shape[0], heads, dh).transpose(0, 1)  # noqa: E731
         o = F.scaled_dot_product_attention(split(q), split(K), split(V))
@@ -438,3 +439,125 @@ def test_strategy_d_needs_initial_full_steps():
             oracle.stack_trajectory(wts["x0"], wts, wl.T, synth.linear_sigmas(wl.T), wl.heads, wl.dh, "f32",
                                     group_sizes=sizes, margin=margin, outside_period=period,
                                     selection=oracle.SELECT_L1REL, iterations=1)
+
+
+# ---------------------------------------------------------------------------
+# RoPE subsampling (Section 2.3)
+# ---------------------------------------------------------------------------
+
+
+def test_rope_bands():
+    assert oracle.rope_bands(128) == (22, 21, 21)
+    assert oracle.rope_bands(64) == (12, 10, 10)
+    assert sum(oracle.rope_bands(128)) * 2 == 128
+
+
+def test_apply_rope_matches_complex_rotation():
+    rng = np.random.default_rng(31)
+    grid, heads, dh = (5, 6, 7), 3, 64
+    pos = rng.integers(0, 5 * 6 * 7, size=50)
+    x = rng.standard_normal((50, heads * dh))
+    ang = oracle.rope_angles(pos, grid, dh)
+    # the angle of pair j of a band: coordinate * theta^(-2j/band_width), from the grid coordinates
+    f, y, w = pos // 42, (pos // 7) % 6, pos % 7
+    nt, nh, nw = oracle.rope_bands(dh)
+    np.testing.assert_allclose(ang[:, 3], f * 10000.0 ** (-6.0 / (2 * nt)), rtol=1e-15)
+    np.testing.assert_allclose(ang[:, nt + 2], y * 10000.0 ** (-4.0 / (2 * nh)), rtol=1e-15)
+    np.testing.assert_allclose(ang[:, nt + nh + 5], w * 10000.0 ** (-10.0 / (2 * nw)), rtol=1e-15)
+    z = torch.view_as_complex(torch.from_numpy(x).reshape(50, heads, dh // 2, 2).contiguous())
+    rot = torch.polar(torch.ones_like(torch.from_numpy(ang)), torch.from_numpy(ang))[:, None, :]
+    ref = torch.view_as_real(z * rot).reshape(50, heads * dh).numpy()
+    np.testing.assert_allclose(oracle.apply_rope(x, ang, heads, dh), ref, rtol=1e-13, atol=1e-14)
+    np.testing.assert_array_equal(oracle.apply_rope(x, np.zeros_like(ang), heads, dh), x)  # position 0
+
+
+def test_rope_scores_depend_on_relative_position():
+    """After the rotation the score of a query and a key depends only on their
+    offset along each axis: shifting both by the same grid offset leaves it."""
+    rng = np.random.default_rng(32)
+    grid, dh = (6, 8, 9), 128
+    q = rng.standard_normal((1, dh))
+    k = rng.standard_normal((1, dh))
+    lin = lambda f, y, x: np.array([(f * 8 + y) * 9 + x])  # noqa: E731
+    score = lambda pq, pk: float((oracle.apply_rope(q, oracle.rope_angles(pq, grid, dh), 1, dh)  # noqa: E731
+                                  @ oracle.apply_rope(k, oracle.rope_angles(pk, grid, dh), 1, dh).T)[0, 0])
+    s0 = score(lin(1, 2, 3), lin(0, 5, 1))
+    assert score(lin(4, 3, 7), lin(3, 6, 5)) == pytest.approx(s0, rel=1e-12)
+    assert score(lin(1, 2, 3), lin(0, 5, 2)) != pytest.approx(s0, rel=1e-6)
+
+
+@pytest.mark.parametrize("name", ["tiny_stack_f32", "tiny_block_f32"])
+def test_rope_iteration_uses_token_positions(name):
+    """With RoPE the HSA iteration on a partial active set equals the torch
+    reference in which every Q/K row is rotated by its token's grid position
+    (the subsampled positional frequencies), not by its place among the
+    active rows."""
+    wl = synth.WORKLOADS[name]
+    wts = synth.draw_stack(wl, seed=41)
+    st = synth.draw_stack_state(wl, seed=42)
+    budget = synth.assign_budgets(st["v_hat"], wl.groups)
+    pos = np.random.default_rng(43).permutation(wl.N)  # tokens in a shuffled sequence order
+    rope = {"grid": wl.grid, "pos": pos}
+    state = {"x": st["x"].astype(np.float64), "v_hat": st["v_hat"].astype(np.float64), "budget": budget,
+             "caches": [(k.astype(np.float64), v.astype(np.float64)) for k, v in st["caches"]]}
+    sig = synth.linear_sigmas(wl.T)
+    r = oracle.stack_iteration(state, wts, 1, wl.T, sig, wl.heads, wl.dh, "f32", rope=rope)
+    idx = oracle.active_set(budget, wl.T, 1)
+    ang = torch.from_numpy(oracle.rope_angles(pos[idx], wl.grid, wl.dh))
+    rot = lambda t: torch.view_as_real(  # noqa: E731
+        torch.view_as_complex(t.reshape(t.shape[0], wl.heads, wl.dh // 2, 2).contiguous())
+        * torch.polar(torch.ones_like(ang), ang)[:, None, :]).reshape(t.shape[0], -1)
+    x, vh, v, caches = _torch_iteration(st["x"], st["v_hat"], st["caches"], wts, idx, wl.heads, wl.dh,
+                                        oracle.euler_delta(sig[1], sig[2]), rotate=rot)
+    tol = dict(rtol=1e-5, atol=1e-6)
+    np.testing.assert_allclose(r["v_fresh"], v, **tol)
+    np.testing.assert_allclose(r["x"], x, **tol)
+    for (k, vv), (kt, vt) in zip(r["caches"], caches):
+        np.testing.assert_allclose(k, kt, **tol)
+        np.testing.assert_allclose(vv, vt, **tol)
+    # rotating by the compact row number instead is a different result
+    r2 = oracle.stack_iteration(state, wts, 1, wl.T, sig, wl.heads, wl.dh, "f32",
+                                rope={"grid": wl.grid, "pos": np.arange(wl.N)})
+    assert np.abs(r2["v_fresh"] - r["v_fresh"]).max() > 1e-4
+
+
+# ---------------------------------------------------------------------------
+# Token reordering (Section 2.5)
+# ---------------------------------------------------------------------------
+
+
+def test_reorder_plan_partition():
+    b = np.array([40, 10, 40, 5, 20, 40, 10])
+    perm, n_cached = oracle.reorder_plan(b, 40)
+    np.testing.assert_array_equal(perm, [1, 3, 4, 6, 0, 2, 5])
+    assert n_cached == 4
+    assert np.all(b[perm[:n_cached]] < 40) and np.all(b[perm[n_cached:]] == 40)
+    _, n0 = oracle.reorder_plan(np.array([20, 5, 20]), 40)  # no baseline group: everything is cached
+    assert n0 == 3
+
+
+def test_reordered_trajectory_is_the_permuted_trajectory():
+    """Reordering the tokens once before the loop, with their grid positions
+    carried along for RoPE, changes nothing but the order: the reordered
+    trajectory is the original one permuted, and the baseline tokens are
+    active at every iteration."""
+    wl = synth.WORKLOADS["tiny_block_f32"]
+    wts = synth.draw_stack(wl, seed=51)
+    budget = synth.assign_budgets(np.zeros((wl.N, 1), np.float32), wl.groups, "first_frame",
+                                  frame_tokens=wl.grid[1] * wl.grid[2], seed=52)
+    sig = synth.linear_sigmas(wl.T)
+    st0 = oracle.initial_state(wts["x0"], wl.layers, wl.d, wl.T)
+    st0["budget"] = budget
+    base = oracle.stack_trajectory(None, wts, wl.T, sig, wl.heads, wl.dh, "f32", state=st0,
+                                   rope={"grid": wl.grid, "pos": None})
+    perm, n_cached = oracle.reorder_plan(budget, wl.T)
+    st1 = oracle.initial_state(wts["x0"][perm], wl.layers, wl.d, wl.T)
+    st1["budget"] = budget[perm]
+    reo = oracle.stack_trajectory(None, wts, wl.T, sig, wl.heads, wl.dh, "f32", state=st1,
+                                  rope={"grid": wl.grid, "pos": perm})
+    for a, b in zip(base, reo):
+        np.testing.assert_array_equal(np.sort(perm[b["idx"]]), a["idx"])
+        assert np.all(np.isin(np.arange(n_cached, wl.N), b["idx"]))  # the baseline suffix is always active
+        np.testing.assert_allclose(b["x"], a["x"][perm], rtol=1e-6, atol=1e-7)
+        for (k0, _), (k1, _) in zip(a["caches"], b["caches"]):
+            np.testing.assert_allclose(k1, k0[perm], rtol=1e-6, atol=1e-7)
