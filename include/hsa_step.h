@@ -283,6 +283,23 @@ int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channels, int32
                        hipStream_t stream);
 
 /*
+ * Rotary-embedding table for the stack (Section 2.3: the positional
+ * frequencies are subsampled to the active set, i.e. every active row is
+ * rotated by its own token's grid position). A head of head_dim channels is
+ * cut into a temporal band of head_dim - 4 floor(head_dim/6) channels and
+ * two spatial bands of 2 floor(head_dim/6) channels; pair j of a band of b
+ * channels at coordinate c turns by c * theta^(-2j/b). The HOST table has
+ * (grid_f + grid_h + grid_w) rows of head_dim/2 (cos, sin) float pairs: row
+ * c holds frame c, row grid_f + c grid row c, row grid_f + grid_h + c grid
+ * column c; entries of pairs outside the row's band are 0. Computed in double
+ * precision, stored in float. hsa_rope_table_floats gives the float count
+ * (0 for invalid sizes).
+ */
+size_t hsa_rope_table_floats(int32_t head_dim, int32_t grid_f, int32_t grid_h, int32_t grid_w);
+int hsa_rope_table(float theta, int32_t head_dim, int32_t grid_f, int32_t grid_h, int32_t grid_w,
+                   float* table_host);
+
+/*
  * Strategy D accumulation (Appendix B, Eq. 7), for every token t:
  *   first != 0:  acc[t] = 0;
  *   first == 0:  acc[t] += (sum_c |v[t][c] - v_prev[t][c]|) / (sum_c |v[t][c]|),
@@ -346,6 +363,11 @@ typedef struct hsa_stack {
                                      W1 [ffn_dim, d], W2 [d, ffn_dim] of each layer */
   void* f;                        /* scratch [N, ffn_dim] dtype when ffn_dim > 0 */
   float* v_prev;                  /* scratch [N, C] fp32 (HSA_SELECT_L1_REL) */
+  /* rotary embedding of Q and K (NULL rope_cs: none) */
+  const float* rope_cs;           /* device copy of the hsa_rope_table of (head_dim, grid) */
+  const int32_t* pos;             /* [N] grid position of every token (NULL: the token index) */
+  int32_t grid_f, grid_h, grid_w; /* latent grid in tokens; grid_f * grid_h * grid_w >= N */
+  int32_t reserved2;              /* 0 */
 } hsa_stack;
 
 /*
@@ -353,7 +375,8 @@ typedef struct hsa_stack {
  *   1. A_i from the budgets (and the margin and outside period of Section
  *      2.5), as hsa_build_active_set_window; |A_i| is copied to the host (one
  *      stream synchronization per iteration);
- *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of rms(h), cache rows
+ *   2. h = embed(dtype(x[A_i])); for each layer: Q/K/V of rms(h) (Q and K
+ *      rotated by their tokens' grid positions when rope_cs is set), cache rows
  *      A_i overwritten, attention of the |A_i| queries against all N cached
  *      rows (scale 1/sqrt(head_dim)), h <- h + O Wo^T; with ctx_len > 0
  *      h <- h + CrossAttn(rms(h) Wq_c^T, K_c, V_c) Wo_c^T; with ffn_dim > 0

@@ -12,6 +12,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // 16 raw bytes
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin over them
@@ -87,7 +88,39 @@ struct RowGemm {
   int c_f32;               // bf16 inputs, fp32 output (no residual)
   const float* row_scale;  // null, or one factor per product row m < M
   int gelu;                // apply the tanh GELU after the row scale (no residual)
+  // Rotary embedding of the outputs z with bit z of rope_outs set: row m is
+  // token rope_tok[m] at grid position p = rope_pos[token] (the token itself
+  // if null; outside [0, F*H*W) reads as 0), coordinates (p / (H*W),
+  // (p / W) % H, p % W). Channel pair k of a head of rope_dh channels lies in
+  // the temporal band (k < nt), the row band (k < nt + nh) or the column
+  // band; its (cos, sin) is rope_cs[r * rope_dh/2 + k] with r the frame,
+  // F + row or F + H + column. Applied after the row scale, before rounding.
+  const f32x2* rope_cs;
+  const int32_t* rope_tok;
+  const int32_t* rope_pos;
+  int rope_outs, rope_dh, rope_nt, rope_nh, rope_f, rope_h, rope_w;
 };
+
+// Grid coordinates of row m's token for the rotary embedding of g.
+struct RopeRow {
+  int f, y, x;
+};
+__device__ __forceinline__ RopeRow rope_row(const RowGemm& g, int m) {
+  const int tok = g.rope_tok[m];
+  const int hw = g.rope_h * g.rope_w;
+  int p = g.rope_pos ? g.rope_pos[tok] : tok;
+  if (p < 0 || p >= g.rope_f * hw) p = 0;
+  return {p / hw, (p / g.rope_w) % g.rope_h, p % g.rope_w};
+}
+
+// The channel pair (a, b) at head-local pair index k, rotated.
+__device__ __forceinline__ f32x2 rope_pair(const RowGemm& g, const RopeRow& r, int k, float a,
+                                           float b) {
+  const int row = k < g.rope_nt ? r.f
+                  : (k < g.rope_nt + g.rope_nh ? g.rope_f + r.y : g.rope_f + g.rope_h + r.x);
+  const f32x2 cs = g.rope_cs[row * (g.rope_dh >> 1) + k];
+  return (f32x2){a * cs[0] - b * cs[1], a * cs[1] + b * cs[0]};
+}
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s);
 
 // Output z of a RowGemm, selected field by field so that a kernel never

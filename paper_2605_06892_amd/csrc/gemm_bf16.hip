@@ -185,6 +185,9 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
     if (crow < 0 || crow >= oz.c_limit) continue;
     const long obase = (long)crow * g.ldc;
     const float rs = g.row_scale ? g.row_scale[m] : 1.f;
+    const bool rope = g.rope_cs && ((g.rope_outs >> z) & 1);
+    RopeRow rr{0, 0, 0};
+    if (rope) rr = rope_row(g, m);
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
 #pragma unroll
@@ -194,6 +197,12 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
           f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                      acc[i][j][4 * q + 3]};
           if (g.row_scale) v *= rs;
+          if (rope) {
+            const int k = (n % g.rope_dh) >> 1;
+            const f32x2 r0 = rope_pair(g, rr, k, v[0], v[1]);
+            const f32x2 r1 = rope_pair(g, rr, k + 1, v[2], v[3]);
+            v = (f32x4){r0[0], r0[1], r1[0], r1[1]};
+          }
           if constexpr (EPI == kEpiF32) {
             *reinterpret_cast<f32x4*>(static_cast<float*>(oz.C) + obase + n) = v;
           } else {

@@ -79,14 +79,28 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
     const int crow = c_rows ? c_rows[m] : m;
     if (crow < 0 || crow >= oz.c_limit) continue;
     const float rs = g.row_scale ? g.row_scale[m] : 1.f;
+    float v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = g.row_scale ? acc[i][j] * rs : acc[i][j];
+      if (g.gelu) v[j] = gelu_tanh(v[j]);
+    }
+    if (g.rope_cs && ((g.rope_outs >> z) & 1)) {  // pairs (n, n+1), (n+2, n+3) of a 4-aligned run
+      const RopeRow rr = rope_row(g, m);
+      const int k = ((tn * TN + tx * 4) % g.rope_dh) >> 1;
+      const f32x2 r0 = rope_pair(g, rr, k, v[0], v[1]);
+      const f32x2 r1 = rope_pair(g, rr, k + 1, v[2], v[3]);
+      v[0] = r0[0];
+      v[1] = r0[1];
+      v[2] = r1[0];
+      v[3] = r1[1];
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = tn * TN + tx * 4 + j;
       if (n < g.Nc) {
         const long e = (long)crow * g.ldc + n;
-        float v = g.row_scale ? acc[i][j] * rs : acc[i][j];
-        if (g.gelu) v = gelu_tanh(v);
-        C[e] = R ? v + R[e] : v;
+        C[e] = R ? v[j] + R[e] : v[j];
       }
     }
   }

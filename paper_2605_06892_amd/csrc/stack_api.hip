@@ -174,6 +174,43 @@ HSA_API int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channel
                                                   static_cast<double*>(workspace), budget, stream));
 }
 
+HSA_API size_t hsa_rope_table_floats(int32_t head_dim, int32_t grid_f, int32_t grid_h,
+                                     int32_t grid_w) {
+  if (head_dim < 6 || head_dim % 2 || grid_f < 1 || grid_h < 1 || grid_w < 1) return 0;
+  return (size_t)(grid_f + grid_h + grid_w) * head_dim;
+}
+
+HSA_API int hsa_rope_table(float theta, int32_t head_dim, int32_t grid_f, int32_t grid_h,
+                           int32_t grid_w, float* table_host) {
+  if (!hsa_rope_table_floats(head_dim, grid_f, grid_h, grid_w) || !(theta > 1.f) ||
+      !isfinite(theta))
+    return HSA_STEP_ERR_SHAPE;
+  if (!table_host) return HSA_STEP_ERR_NULL;
+  const int half = head_dim / 2, sp = head_dim / 6;
+  const int band_pairs[3] = {(head_dim - 4 * sp) / 2, sp, sp};
+  const int band_rows[3] = {grid_f, grid_h, grid_w};
+  int row0 = 0, pair0 = 0;
+  for (int b = 0; b < 3; ++b) {
+    for (int c = 0; c < band_rows[b]; ++c) {
+      float* row = table_host + (size_t)(row0 + c) * head_dim;
+      for (int k = 0; k < half; ++k) {
+        const int j = k - pair0;
+        double cs = 0.0, sn = 0.0;
+        if (j >= 0 && j < band_pairs[b]) {
+          const double ang = c * pow((double)theta, -2.0 * j / (2.0 * band_pairs[b]));
+          cs = cos(ang);
+          sn = sin(ang);
+        }
+        row[2 * k] = (float)cs;
+        row[2 * k + 1] = (float)sn;
+      }
+    }
+    row0 += band_rows[b];
+    pair0 += band_pairs[b];
+  }
+  return HSA_STEP_OK;
+}
+
 HSA_API int hsa_l1_rel_accumulate(const float* v, float* v_prev, int64_t n_tokens,
                                   int32_t channels, double* acc, int32_t first,
                                   hipStream_t stream) {
@@ -213,8 +250,13 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   const int L = s->n_layers, C = s->channels, dh = s->head_dim;
   const int F = s->ffn_dim, Lc = s->ctx_len;
   if (N < 1 || N > kMaxRows || L < 0 || s->heads <= 0 || (dh != 64 && dh != 128) || C <= 0 ||
-      s->reserved != 0 || (int64_t)s->heads * dh > INT32_MAX / 4 || F < 0 || Lc < 0 ||
-      Lc > kMaxRows)
+      s->reserved != 0 || s->reserved2 != 0 || (int64_t)s->heads * dh > INT32_MAX / 4 || F < 0 ||
+      Lc < 0 || Lc > kMaxRows)
+    return HSA_STEP_ERR_SHAPE;
+  const bool rope = s->rope_cs != nullptr;
+  if (rope && (s->grid_f < 1 || s->grid_h < 1 || s->grid_w < 1 ||
+               (int64_t)s->grid_f * s->grid_h * s->grid_w < N ||
+               (int64_t)s->grid_f * s->grid_h * s->grid_w > kMaxRows))
     return HSA_STEP_ERR_SHAPE;
   const int d = s->heads * dh;
   if (s->dtype == HSA_STEP_BF16 && (C % 64 != 0 || F % 64 != 0)) return HSA_STEP_ERR_SHAPE;
@@ -261,10 +303,16 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
     weights.push_back({wc[3], (size_t)Lc * row_d});
   }
   for (int i = 0; i < 2 * L && F > 0; ++i) weights.push_back({s->w_ffn[i], (size_t)F * row_d});
+  if (rope) {
+    weights.push_back({s->rope_cs, hsa_rope_table_floats(dh, s->grid_f, s->grid_h, s->grid_w) * 4});
+    if (s->pos) weights.push_back({s->pos, (size_t)N * 4});
+  }
   for (const Span& b : written)
     if (!aligned(b.p, 16)) return HSA_STEP_ERR_SHAPE;
-  for (const Span& b : weights)
-    if (!aligned(b.p, 16)) return HSA_STEP_ERR_SHAPE;
+  for (const Span& b : weights) {
+    const bool table = rope && (b.p == s->rope_cs || b.p == s->pos);
+    if (!aligned(b.p, table ? 8 : 16)) return HSA_STEP_ERR_SHAPE;
+  }
   if (any_overlap(written) || any_overlap(written, weights)) return HSA_STEP_ERR_ALIAS;
 
   // 1. active set and its size on the host
@@ -312,6 +360,18 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       g.out[2] = {w[2], vc, s->idx, (int)N};
       g.n_out = 3;
       g.row_scale = s->row_scale;
+      if (rope) {
+        g.rope_cs = reinterpret_cast<const hsa::f32x2*>(s->rope_cs);
+        g.rope_tok = s->idx;
+        g.rope_pos = s->pos;
+        g.rope_outs = 3;  // Q and K
+        g.rope_dh = dh;
+        g.rope_nt = (dh - 4 * (dh / 6)) / 2;
+        g.rope_nh = dh / 6;
+        g.rope_f = s->grid_f;
+        g.rope_h = s->grid_h;
+        g.rope_w = s->grid_w;
+      }
       if (!rms() || !gemm(g) || !attend(s->q, kc, vc, (int)N) ||
           !gemm(compact_gemm(s->o, n, d, w[3], d, nullptr, s->h, false, s->h)))
         return HSA_STEP_ERR_LAUNCH;

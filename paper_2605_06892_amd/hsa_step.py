@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
             "hsa_row_rms_scale": (ctypes.c_int, [ctypes.c_int, P, I32, I32, F, P, P]),
             "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, P, I32, ctypes.c_int, P, P]),
             "hsa_l1_rel_accumulate": (ctypes.c_int, [P, P, I64, I32, P, I32, P]),
+            "hsa_rope_table_floats": (S, [I32, I32, I32, I32]),
+            "hsa_rope_table": (ctypes.c_int, [F, I32, I32, I32, I32, P]),
             "hsa_assign_budgets_by_key": (ctypes.c_int, [P, I64, I32, P, P, I32, P, P]),
             "hsa_assign_budgets_workspace_bytes": (S, [I64]),
             "hsa_assign_budgets": (ctypes.c_int, [P, I64, I32, I32, P, P, I32, P, P, S, P]),
@@ -94,6 +96,8 @@ EXPORTED = (
     "hsa_assign_budgets",
     "hsa_l1_rel_accumulate",
     "hsa_assign_budgets_by_key",
+    "hsa_rope_table_floats",
+    "hsa_rope_table",
     "hsa_stack_iteration",
 )
 
@@ -117,6 +121,9 @@ class HsaStack(ctypes.Structure):
         ("ffn_dim", ctypes.c_int32), ("ctx_len", ctypes.c_int32),
         ("w_cross", ctypes.POINTER(ctypes.c_void_p)), ("w_ffn", ctypes.POINTER(ctypes.c_void_p)),
         ("f", ctypes.c_void_p), ("v_prev", ctypes.c_void_p),
+        ("rope_cs", ctypes.c_void_p), ("pos", ctypes.c_void_p),
+        ("grid_f", ctypes.c_int32), ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32),
+        ("reserved2", ctypes.c_int32),
     ]
 
 
@@ -301,15 +308,27 @@ def hsa_assign_budgets_by_key(keys, T: int, group_sizes, budget, stream=None) ->
     _check("hsa_assign_budgets_by_key", st)
 
 
+def hsa_rope_table(theta: float, head_dim: int, grid) -> torch.Tensor:
+    """The (cos, sin) table of the stack's rotary embedding, on the host
+    (float32 [(F + H + W), head_dim])."""
+    n = int(lib().hsa_rope_table_floats(head_dim, *grid))
+    if n == 0:
+        raise ValueError("invalid rotary table sizes")
+    out = torch.empty(n, dtype=torch.float32)
+    _check("hsa_rope_table", lib().hsa_rope_table(theta, head_dim, *grid, ctypes.c_void_p(out.data_ptr())))
+    return out.view(-1, head_dim)
+
+
 def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_active, xa, h, q, o, v_fresh,
                keys, row_scale, heads: int, head_dim: int, cross=None, ffn=None, f=None,
-               v_prev=None) -> HsaStack:
+               v_prev=None, rope_cs=None, pos=None, grid=(0, 0, 0)) -> HsaStack:
     """Fill a struct hsa_stack from device tensors. layers: per layer
     (wq, wk, wv, wo); caches: per layer (k_hat, v_hat); cross: per layer
     (wq_c, wo_c, k_c, v_c) or None; ffn: per layer (w1, w2) or None. The
     returned struct keeps its host pointer arrays alive; the tensors must
     outlive it."""
-    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale, f, v_prev]
+    ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale, f, v_prev,
+          rope_cs, pos]
     ts += [t for lw in layers for t in lw] + [t for c in caches for t in c]
     ts += [t for lw in (cross or ()) for t in lw] + [t for lw in (ffn or ()) for t in lw]
     _dev(*ts)
@@ -327,7 +346,9 @@ def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_acti
                  o=o.data_ptr(), v_fresh=v_fresh.data_ptr(), keys=keys.data_ptr(),
                  row_scale=row_scale.data_ptr(), ffn_dim=0 if not ffn else ffn[0][0].shape[0],
                  ctx_len=0 if not cross else cross[0][2].shape[0],
-                 f=0 if f is None else f.data_ptr(), v_prev=0 if v_prev is None else v_prev.data_ptr())
+                 f=0 if f is None else f.data_ptr(), v_prev=0 if v_prev is None else v_prev.data_ptr(),
+                 rope_cs=0 if rope_cs is None else rope_cs.data_ptr(), pos=0 if pos is None else pos.data_ptr(),
+                 grid_f=grid[0], grid_h=grid[1], grid_w=grid[2], reserved2=0)
     keep = [wl, cl]
     if cross:
         xl = (ctypes.c_void_p * (4 * len(cross)))(*[t.data_ptr() for lw in cross for t in lw])

@@ -42,6 +42,9 @@ class StackBuffers:
     cross: list | None = None   # per layer (wq_c, wo_c, k_c, v_c); k_c, v_c [ctx, d]
     ffn: list | None = None     # per layer (w1 [F, d], w2 [d, F])
     f: torch.Tensor | None = None  # [N, F]
+    rope_cs: torch.Tensor | None = None  # rotary (cos, sin) table on the device
+    pos: torch.Tensor | None = None      # int32 [N] grid position of every token
+    grid: tuple = (0, 0, 0)
     _handle: H.HsaStack | None = field(default=None, repr=False)
 
     @property
@@ -76,6 +79,15 @@ class StackBuffers:
                    ffn=[(e(ffn, d), e(d, ffn)) for _ in range(n_layers)] if ffn else None,
                    f=e(N, ffn) if ffn else None)
 
+    def enable_rope(self, grid, theta: float = 10000.0, pos: torch.Tensor | None = None) -> None:
+        """Rotate Q and K by the tokens' positions in the latent grid (F, H, W)
+        (Section 2.3: the positional frequencies follow the active set). pos:
+        the grid position of every token, identity if None."""
+        self.rope_cs = H.hsa_rope_table(theta, self.head_dim, grid).to(self.x.device)
+        self.pos = pos
+        self.grid = tuple(int(g) for g in grid)
+        self._handle = None
+
     def set_context(self, ctx: torch.Tensor, wk_c, wv_c) -> None:
         """K_c = ctx Wk_c^T and V_c = ctx Wv_c^T of every layer, computed once
         per sample on the device (hsa_linear)."""
@@ -91,7 +103,8 @@ class StackBuffers:
                                         n_active=self.n_active, xa=self.xa, h=self.h, q=self.q, o=self.o,
                                         v_fresh=self.v_fresh, keys=self.keys, row_scale=self.row_scale,
                                         heads=self.heads, head_dim=self.head_dim, cross=self.cross,
-                                        ffn=self.ffn, f=self.f, v_prev=self.v_prev)
+                                        ffn=self.ffn, f=self.f, v_prev=self.v_prev, rope_cs=self.rope_cs,
+                                        pos=self.pos, grid=self.grid)
         return self._handle
 
 

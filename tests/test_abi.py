@@ -311,3 +311,27 @@ def test_l1_rel_and_key_assignment_errors(lib):
     assert g(None, 100, 40, gb, gs, 2, B, None) == NULL
     assert g(A, 100, 40, gb, gs, 2, A + 16, None) == ALIAS
     assert g(A + 4, 100, 40, gb, gs, 2, B, None) == SHAPE
+
+
+def test_rope_table_matches_the_oracle_angles(lib):
+    """The host-side rotary table holds cos/sin of the oracle's angles (within
+    fp32 rounding) for every coordinate of its band, zeros elsewhere."""
+    import numpy as np
+
+    import oracle
+    for dh, grid in ((128, (21, 30, 52)), (64, (3, 10, 10))):
+        t = H.hsa_rope_table(10000.0, dh, grid).numpy().reshape(sum(grid), dh // 2, 2)
+        F, Hh, W = grid
+        nt, nh, nw = oracle.rope_bands(dh)
+        for band, (lo, n, pairs) in enumerate(((0, F, range(0, nt)), (F, Hh, range(nt, nt + nh)),
+                                                 (F + Hh, W, range(nt + nh, nt + nh + nw)))):
+            coord = np.arange(n)
+            p = [coord * Hh * W, coord * W, coord][band]  # a position with this coordinate, others 0
+            ang = oracle.rope_angles(p, grid, dh)[:, list(pairs)]
+            np.testing.assert_allclose(t[lo:lo + n, list(pairs), 0], np.cos(ang), rtol=0, atol=2e-7)
+            np.testing.assert_allclose(t[lo:lo + n, list(pairs), 1], np.sin(ang), rtol=0, atol=2e-7)
+            others = [k for k in range(dh // 2) if k not in pairs]
+            assert np.all(t[lo:lo + n, others] == 0)
+    assert lib.hsa_rope_table_floats(128, 0, 30, 52) == 0
+    assert lib.hsa_rope_table(10000.0, 128, 2, 2, 2, None) == NULL
+    assert lib.hsa_rope_table(0.5, 128, 2, 2, 2, A) == SHAPE

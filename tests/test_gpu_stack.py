@@ -179,9 +179,11 @@ def test_assign_budgets_rejects_bad_groups():
 # ---------------------------------------------------------------------------
 
 
-def _upload(wl, wts, N, L, state=None):
+def _upload(wl, wts, N, L, state=None, rope_pos=None):
     b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch_dtype(wl.dtype),
                                 ffn=wl.ffn, ctx=wl.ctx)
+    if rope_pos is not None:
+        b.enable_rope(wl.grid, pos=i32(rope_pos))
     b.w_embed.copy_(to_dev(wts["w_embed"], wl.dtype))
     b.w_head.copy_(to_dev(wts["w_head"], wl.dtype))
     for dst, lw in zip(b.layers, wts["layers"]):
@@ -214,17 +216,21 @@ def _upload(wl, wts, N, L, state=None):
     return b
 
 
-@pytest.mark.parametrize("name,margin,selection", [("tiny_stack_f32", 0, "norm"), ("tiny_block_f32", 0, "norm"),
-                                                    ("tiny_stack_f32", 2, "l1rel"), ("tiny_block_f32", 3, "l1rel")])
-def test_tiny_f32_stack_trajectory(name, margin, selection):
+@pytest.mark.parametrize("name,margin,selection,rope", [
+    ("tiny_stack_f32", 0, "norm", False), ("tiny_block_f32", 0, "norm", False),
+    ("tiny_stack_f32", 2, "l1rel", False), ("tiny_block_f32", 3, "l1rel", False),
+    ("tiny_stack_f32", 0, "norm", True), ("tiny_block_f32", 2, "l1rel", True)])
+def test_tiny_f32_stack_trajectory(name, margin, selection, rope):
     wl = synth.WORKLOADS[name]
     wts = synth.draw_stack(wl, seed=0)
     sizes = synth.group_sizes(wl.N, wl.groups)
     sig = synth.linear_sigmas(wl.T)
+    pos = np.random.default_rng(9).permutation(wl.N).astype(np.int32) if rope else None
     recs = oracle.stack_trajectory(wts["x0"], wts, wl.T, sig, wl.heads, wl.dh, "f32", group_sizes=sizes,
-                                   margin=margin, selection=selection)
+                                   margin=margin, selection=selection,
+                                   rope={"grid": wl.grid, "pos": pos} if rope else None)
     sel = H.SELECT_L1_REL if selection == "l1rel" else H.SELECT_VELOCITY_NORM
-    b = _upload(wl, wts, wl.N, wl.layers)
+    b = _upload(wl, wts, wl.N, wl.layers, rope_pos=pos)
     for r in recs:
         keys = r["l1"] if selection == "l1rel" else oracle.velocity_keys(r["v_hat"])
         n, refreshed = S.iteration(b, wl.T, r["i"], sig, sizes, margin=margin, selection=sel)
@@ -248,9 +254,10 @@ def _state_for(wl, seed, N, L):
     return st
 
 
-@pytest.mark.parametrize("name", ["small_stack_bf16", "small_block_bf16"])
+@pytest.mark.parametrize("name,rope", [("small_stack_bf16", False), ("small_block_bf16", False),
+                                       ("small_block_bf16", True)])
 @pytest.mark.parametrize("iteration", [1, 2, 0])  # 25% active, 50% active, all active + refresh
-def test_small_bf16_stack_iteration(iteration, name):
+def test_small_bf16_stack_iteration(iteration, name, rope):
     wl = synth.WORKLOADS[name]
     N, L = wl.N, wl.layers
     wts = synth.draw_stack(wl, seed=31)
@@ -260,8 +267,10 @@ def test_small_bf16_stack_iteration(iteration, name):
     state = {"x": st["x"].astype(np.float64), "v_hat": st["v_hat"].astype(np.float64),
              "budget": st["budget"],
              "caches": [(k.astype(np.float64), v.astype(np.float64)) for k, v in st["caches"]]}
-    r = oracle.stack_iteration(state, wts, iteration, wl.T, sig, wl.heads, wl.dh, "bf16", sizes)
-    b = _upload(wl, wts, N, L, st)
+    pos = np.random.default_rng(10).permutation(N).astype(np.int32) if rope else None
+    r = oracle.stack_iteration(state, wts, iteration, wl.T, sig, wl.heads, wl.dh, "bf16", sizes,
+                               rope={"grid": wl.grid, "pos": pos} if rope else None)
+    b = _upload(wl, wts, N, L, st, rope_pos=pos)
     caches_before = [(host_bits(k), host_bits(v)) for k, v in b.caches]
     n, refreshed = S.iteration(b, wl.T, iteration, sig, sizes)
     assert (n, refreshed) == (r["idx"].size, r["refreshed"])
