@@ -300,6 +300,28 @@ int hsa_rope_table(float theta, int32_t head_dim, int32_t grid_f, int32_t grid_h
                    float* table_host);
 
 /*
+ * Token reordering (Section 2.5): perm receives the tokens with budget < T
+ * followed by those with budget T (the baseline group, active at every
+ * iteration), each part in index order; *n_lead = the count of the former,
+ * i.e. the cache rows a reordered stack needs. Invalid budgets give
+ * n_lead = -1 (and HSA_STEP_ERR_BUDGET with n_lead_host). perm and n_lead_dev
+ * are device int32 ([n_tokens], [1]); n_lead_host, if not NULL, is filled
+ * after one stream synchronization.
+ */
+int hsa_reorder_plan(const int32_t* budget, int64_t n_tokens, int32_t T, int32_t* perm,
+                     int32_t* n_lead_dev, int32_t* n_lead_host, hipStream_t stream);
+
+/*
+ * Row permutation of token-indexed state: dst[i] = src[perm[i]] for
+ * i < n_rows, or with inverse != 0, dst[perm[i]] = src[i] (undoing the
+ * reordering before the latent leaves the sampler). Rows are row_bytes wide;
+ * perm entries outside [0, n_rows) skip their row. src and dst must not
+ * overlap.
+ */
+int hsa_permute_rows(const void* src, const int32_t* perm, int64_t n_rows, int64_t row_bytes,
+                     int32_t inverse, void* dst, hipStream_t stream);
+
+/*
  * Strategy D accumulation (Appendix B, Eq. 7), for every token t:
  *   first != 0:  acc[t] = 0;
  *   first == 0:  acc[t] += (sum_c |v[t][c] - v_prev[t][c]|) / (sum_c |v[t][c]|),
@@ -368,6 +390,16 @@ typedef struct hsa_stack {
   const int32_t* pos;             /* [N] grid position of every token (NULL: the token index) */
   int32_t grid_f, grid_h, grid_w; /* latent grid in tokens; grid_f * grid_h * grid_w >= N */
   int32_t reserved2;              /* 0 */
+  /* prefix-only KV cache of reordered tokens (Section 2.5) */
+  int32_t prefix_cache;           /* 1: tokens n_cached .. N-1 are the baseline group (budget T,
+                                     active at every iteration, as after hsa_reorder_plan and
+                                     hsa_permute_rows); each layer's K_hat/V_hat then has only
+                                     n_cached rows and the baseline rows' fresh keys and values
+                                     live in k_tail/v_tail. Needs n_groups == 0 (fixed groups). */
+  int32_t reserved3;              /* 0 */
+  int64_t n_cached;               /* 0 .. N (prefix_cache only) */
+  void* k_tail;                   /* scratch [N - n_cached, d] dtype shared by the layers */
+  void* v_tail;
 } hsa_stack;
 
 /*
@@ -400,6 +432,8 @@ typedef struct hsa_stack {
  * Iteration 0 activates every token whatever the budgets are, which fills
  * every cache and the velocity cache; later iterations read cache rows
  * written earlier. n_groups == 0 and every budget T is the dense loop.
+ * With prefix_cache, an iteration whose active set does not contain every
+ * token from n_cached on returns HSA_STEP_ERR_BUDGET before the stack runs.
  *   n_active_host   if not NULL: |A_i|
  *   refreshed_host  if not NULL: 1 if the budgets were reassigned, else 0
  * Writable buffers must not overlap each other or any weight.

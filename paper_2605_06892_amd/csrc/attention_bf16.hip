@@ -14,7 +14,9 @@
 // XOR with a function of the row (K: f(r) = ((r&3)<<2)|((r>>2)&3) for 128-wide
 // heads; V: f(r) = (r&3)<<2), so that the K fragment reads (16 rows, one chunk)
 // and the V transpose reads (4 rows, 4 chunks) both hit disjoint LDS banks.
-// Rows beyond N are loaded from row N-1 and masked out of the softmax.
+// Rows beyond N are loaded from row N-1 and masked out of the softmax. The N
+// rows may come in two segments: a cache prefix and, from row n_split on,
+// fresh rows of a second buffer (the prefix-only cache of reordered tokens).
 //
 // Keys are consumed in 32-row blocks. Per block:
 //   S^T = K Q^T - m   v_mfma_f32_32x32x16_bf16 with K rows as the A operand
@@ -73,7 +75,8 @@ __device__ __forceinline__ int swz_v(int r) {
 template <int DH, int NW>
 __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
-    bf16* __restrict__ o, int n_q, int n_kv, int d, float sl2e, int n_qtiles) {
+    bf16* __restrict__ o, int n_q, int n_kv, int d, float sl2e, int n_qtiles,
+    const bf16* __restrict__ kc2, const bf16* __restrict__ vc2, int n_split) {
   constexpr int BQ = NW * 32;        // queries per workgroup
   constexpr int CPR = DH / 8;        // 16-byte chunks per cached row
   constexpr int RPS = 64 / CPR;      // rows per 1 KB LDS segment
@@ -121,6 +124,8 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   // LDS slot lane%CPR holding global chunk slot ^ f(row)
   const bf16* kg = kc + col0;
   const bf16* vg = vc + col0;
+  const bf16* kg2 = kc2 + col0;  // rows n_split.. (unused when n_split >= n_kv)
+  const bf16* vg2 = vc2 + col0;
   auto issue_tile = [&](auto buf, int kv0) {
     bf16* kd = kbuf(buf);
     bf16* vd = vbuf(buf);
@@ -130,8 +135,10 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
       const int row = seg * RPS + lane / CPR;
       const int slot = lane % CPR;
       const long n = min(kv0 + row, n_kv - 1);
-      const bf16* ks = kg + n * d + (slot ^ swz_k<DH>(row)) * 8;
-      const bf16* vs = vg + n * d + (slot ^ swz_v<DH>(row)) * 8;
+      const bool first = n < n_split;
+      const long r = first ? n : n - n_split;
+      const bf16* ks = (first ? kg : kg2) + r * d + (slot ^ swz_k<DH>(row)) * 8;
+      const bf16* vs = (first ? vg : vg2) + r * d + (slot ^ swz_v<DH>(row)) * 8;
       __builtin_amdgcn_global_load_lds((global_cvoid*)ks, (lds_void*)(kd + seg * 512), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((global_cvoid*)vs, (lds_void*)(vd + seg * 512), 16, 0, 0);
     }
@@ -285,22 +292,30 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
 
 template <int DH, int NW>
 hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
-                      int heads, float sl2e, hipStream_t s) {
+                      int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
+                      int n_split) {
   constexpr int BQ = NW * 32;
   const int n_qtiles = (n_q + BQ - 1) / BQ;
   const int d = heads * DH;
   hipLaunchKernelGGL((attention_bf16_kernel<DH, NW>), dim3((unsigned)(n_qtiles * heads)),
                      dim3(NW * 64), 0, s, static_cast<const bf16*>(q),
                      static_cast<const bf16*>(k), static_cast<const bf16*>(v),
-                     static_cast<bf16*>(o), n_q, n_kv, d, sl2e, n_qtiles);
+                     static_cast<bf16*>(o), n_q, n_kv, d, sl2e, n_qtiles,
+                     static_cast<const bf16*>(k2), static_cast<const bf16*>(v2), n_split);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, void* o, int n_q,
-                                 int n_kv, int heads, int head_dim, float scale, hipStream_t s) {
+                                 int n_kv, int heads, int head_dim, float scale, hipStream_t s,
+                                 const void* k2, const void* v2, int n_split) {
   if (n_q <= 0) return hipSuccess;
+  if (!k2 || !v2) {
+    k2 = k;  // any valid pointer: never read
+    v2 = v;
+    n_split = n_kv;
+  }
   const float sl2e = scale * 1.4426950408889634f;
   // Workgroup shape: 8 waves (two per SIMD, 256 queries) whenever that still
   // gives every CU a workgroup, else 4 waves (128 queries). HSA_ATTN_WAVES
@@ -309,10 +324,10 @@ hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, vo
   int nw = forced ? atoi(forced) : 0;
   if (nw != 4 && nw != 8) nw = ((long)((n_q + 255) / 256) * heads >= 256) ? 8 : 4;
   if (head_dim == 64)
-    return nw == 8 ? launch_cfg<64, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s)
-                   : launch_cfg<64, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
-  return nw == 8 ? launch_cfg<128, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s)
-                 : launch_cfg<128, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s);
+    return nw == 8 ? launch_cfg<64, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split)
+                   : launch_cfg<64, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
+  return nw == 8 ? launch_cfg<128, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split)
+                 : launch_cfg<128, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
 }
 
 }  // namespace hsa

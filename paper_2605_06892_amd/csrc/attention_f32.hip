@@ -17,7 +17,8 @@ constexpr int kWavesPerBlock = kThreads / kWave;
 template <int DH>
 __global__ __launch_bounds__(kThreads) void attention_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
-    float* __restrict__ o, int n_q, int n_kv, int heads, int d, float scale) {
+    float* __restrict__ o, int n_q, int n_kv, int heads, int d, float scale,
+    const float* __restrict__ k2, const float* __restrict__ v2, int n_split) {
   constexpr int R = DH / kWave;  // output channels per lane
   __shared__ float qs[kWavesPerBlock][DH];
   const int lane = threadIdx.x & (kWave - 1);
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(kThreads) void attention_f32_kernel(
     const int n = n0 + lane;
     float s = -INFINITY;
     if (n < n_kv) {
-      const float* kr = k + (long)n * d + col0;
+      const float* kr = (n < n_split ? k + (long)n * d : k2 + (long)(n - n_split) * d) + col0;
       float dot = 0.f;
 #pragma unroll 8
       for (int c = 0; c < DH; ++c) dot = fmaf(qs[w][c], kr[c], dot);
@@ -55,7 +56,8 @@ __global__ __launch_bounds__(kThreads) void attention_f32_kernel(
     const int cnt = min(kWave, n_kv - n0);
     for (int i = 0; i < cnt; ++i) {
       const float pi = __shfl(p, i);
-      const float* vr = v + (long)(n0 + i) * d + col0;
+      const int nv = n0 + i;
+      const float* vr = (nv < n_split ? v + (long)nv * d : v2 + (long)(nv - n_split) * d) + col0;
 #pragma unroll
       for (int r = 0; r < R; ++r) acc[r] = fmaf(pi, vr[lane + kWave * r], acc[r]);
     }
@@ -69,7 +71,9 @@ __global__ __launch_bounds__(kThreads) void attention_f32_kernel(
 }  // namespace
 
 hipError_t launch_attention_f32(const void* q, const void* k, const void* v, void* o, int n_q,
-                                int n_kv, int heads, int head_dim, float scale, hipStream_t s) {
+                                int n_kv, int heads, int head_dim, float scale, hipStream_t s,
+                                const void* k2, const void* v2, int n_split) {
+  if (!k2 || !v2) n_split = n_kv;
   if (n_q <= 0) return hipSuccess;
   const long pairs = (long)n_q * heads;
   const dim3 grid((unsigned)((pairs + kWavesPerBlock - 1) / kWavesPerBlock));
@@ -78,12 +82,14 @@ hipError_t launch_attention_f32(const void* q, const void* k, const void* v, voi
   const float* kf = static_cast<const float*>(k);
   const float* vf = static_cast<const float*>(v);
   float* of = static_cast<float*>(o);
+  const float* k2f = static_cast<const float*>(k2);
+  const float* v2f = static_cast<const float*>(v2);
   if (head_dim == 64)
     hipLaunchKernelGGL(attention_f32_kernel<64>, grid, dim3(kThreads), 0, s, qf, kf, vf, of, n_q,
-                       n_kv, heads, d, scale);
+                       n_kv, heads, d, scale, k2f, v2f, n_split);
   else
     hipLaunchKernelGGL(attention_f32_kernel<128>, grid, dim3(kThreads), 0, s, qf, kf, vf, of, n_q,
-                       n_kv, heads, d, scale);
+                       n_kv, heads, d, scale, k2f, v2f, n_split);
   return hipGetLastError();
 }
 

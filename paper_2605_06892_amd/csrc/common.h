@@ -75,6 +75,8 @@ struct RowGemmOut {
   void* C;
   const int32_t* c_rows;
   int c_limit;
+  void* C2;     // if set: rows crow >= c_split go to C2 row crow - c_split
+  int c_split;
 };
 struct RowGemm {
   const void* A;
@@ -131,14 +133,22 @@ __device__ __forceinline__ RowGemmOut row_gemm_out(const RowGemm& g, int z) {
   o.C = z == 0 ? g.out[0].C : (z == 1 ? g.out[1].C : g.out[2].C);
   o.c_rows = z == 0 ? g.out[0].c_rows : (z == 1 ? g.out[1].c_rows : g.out[2].c_rows);
   o.c_limit = z == 0 ? g.out[0].c_limit : (z == 1 ? g.out[1].c_limit : g.out[2].c_limit);
+  o.C2 = z == 0 ? g.out[0].C2 : (z == 1 ? g.out[1].C2 : g.out[2].C2);
+  o.c_split = z == 0 ? g.out[0].c_split : (z == 1 ? g.out[1].c_split : g.out[2].c_split);
   return o;
 }
 hipError_t launch_row_gemm_f32(const RowGemm& g, hipStream_t s);
 
+// Keys/values: rows n < n_split come from (k, v), rows n_split .. n_kv-1 from
+// (k2, v2) at row n - n_split (a cache prefix followed by fresh rows).
 hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, void* o, int n_q,
-                                 int n_kv, int heads, int head_dim, float scale, hipStream_t s);
+                                 int n_kv, int heads, int head_dim, float scale, hipStream_t s,
+                                 const void* k2 = nullptr, const void* v2 = nullptr,
+                                 int n_split = 0x7fffffff);
 hipError_t launch_attention_f32(const void* q, const void* k, const void* v, void* o, int n_q,
-                                int n_kv, int heads, int head_dim, float scale, hipStream_t s);
+                                int n_kv, int heads, int head_dim, float scale, hipStream_t s,
+                                const void* k2 = nullptr, const void* v2 = nullptr,
+                                int n_split = 0x7fffffff);
 
 hipError_t launch_cached_euler(float* x, float* v_cache, const float* v_fresh,
                                const int32_t* idx, int n_active, long n_tokens, int channels,
@@ -157,6 +167,17 @@ hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active
 // scale[m] = 1 / sqrt(mean_k x[m][k]^2 + eps) for m < n_rows (fp32 sums).
 hipError_t launch_row_rms_scale(const void* x, bool bf16_in, int n_rows, int d, float eps,
                                 float* scale, hipStream_t s);
+
+// Token reordering: perm = tokens with budget < T, then those with budget T
+// (each part in index order); n_lead = number of the former, or -1 if a
+// budget is invalid (1 <= s <= T, T % s == 0).
+hipError_t launch_reorder_plan(const int32_t* budget, int n, int T, int32_t* perm,
+                               int32_t* n_lead, hipStream_t s);
+
+// dst[i] = src[perm[i]] (inverse: dst[perm[i]] = src[i]) for rows of row_bytes;
+// indices outside [0, n_rows) skip the row.
+hipError_t launch_permute_rows(const void* src, const int32_t* perm, long n_rows, long row_bytes,
+                               bool inverse, void* dst, hipStream_t s);
 
 // Budget groups in ascending budget order: group k holds the tokens of rank
 // end[k-1] .. end[k]-1 (end[-1] = 0) and gets step budget budget[k].

@@ -183,7 +183,13 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
     if (m >= g.M) continue;
     const int crow = c_rows ? c_rows[m] : m;
     if (crow < 0 || crow >= oz.c_limit) continue;
-    const long obase = (long)crow * g.ldc;
+    void* cbase = oz.C;
+    long orow = crow;
+    if (oz.C2 && crow >= oz.c_split) {  // rows past the split go to the second buffer
+      cbase = oz.C2;
+      orow = crow - oz.c_split;
+    }
+    const long obase = orow * g.ldc;
     const float rs = g.row_scale ? g.row_scale[m] : 1.f;
     const bool rope = g.rope_cs && ((g.rope_outs >> z) & 1);
     RopeRow rr{0, 0, 0};
@@ -204,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
             v = (f32x4){r0[0], r0[1], r1[0], r1[1]};
           }
           if constexpr (EPI == kEpiF32) {
-            *reinterpret_cast<f32x4*>(static_cast<float*>(oz.C) + obase + n) = v;
+            *reinterpret_cast<f32x4*>(static_cast<float*>(cbase) + obase + n) = v;
           } else {
             if constexpr (EPI == kEpiBf16Residual) {
               const bf16x4 r =
@@ -215,7 +221,7 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
 #pragma unroll
               for (int u = 0; u < 4; ++u) v[u] = gelu_tanh(v[u]);
             }
-            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(oz.C) + obase + n) = to_bf16x4(v);
+            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(cbase) + obase + n) = to_bf16x4(v);
           }
         }
       }

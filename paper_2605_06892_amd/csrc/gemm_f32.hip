@@ -70,6 +70,7 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
   }
 
   float* C = static_cast<float*>(oz.C);  // may alias the residual
+  float* C2 = static_cast<float*>(oz.C2);
   const float* R = static_cast<const float*>(g.residual);
   const int32_t* c_rows = oz.c_rows;
 #pragma unroll
@@ -95,12 +96,18 @@ __global__ __launch_bounds__(kThreads) void row_gemm_f32_kernel(RowGemm g) {
       v[2] = r1[0];
       v[3] = r1[1];
     }
+    float* cb = C;
+    long orow = crow;
+    if (C2 && crow >= oz.c_split) {  // rows past the split go to the second buffer
+      cb = C2;
+      orow = crow - oz.c_split;
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = tn * TN + tx * 4 + j;
       if (n < g.Nc) {
-        const long e = (long)crow * g.ldc + n;
-        C[e] = R ? v[j] + R[e] : v[j];
+        const long e = orow * g.ldc + n;
+        cb[e] = R ? v[j] + R[e] : v[j];
       }
     }
   }

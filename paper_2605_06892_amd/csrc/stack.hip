@@ -16,6 +16,10 @@
 //     over the initial full-budget steps of |v_i - v_{i-1}|_1 / |v_i|_1, the
 //     two L1 norms summed in float64 in channel order, one float64 division
 //     per step; v_{i-1} is kept in a token-major copy.
+//   * reorder_plan_kernel + permute_rows_kernel: token reordering (Section
+//     2.5): non-baseline tokens first, then the baseline group, each part in
+//     index order, and the row permutation that applies it to token-indexed
+//     state (and inverts it at the end).
 //   * row_rms_scale: 1 / sqrt(mean(h^2) + eps) of every compact hidden row, the
 //     RMS normalization before each layer's Q/K/V projections and before the
 //     velocity head. A per-row factor commutes with the projection, so the
@@ -180,6 +184,87 @@ __global__ __launch_bounds__(kThreads) void rank_budgets(const unsigned long lon
   }
 }
 
+// Token reordering plan: one workgroup walks the budgets twice in chunks of
+// 1024 x 16 tokens, a wave prefix sum per chunk giving each thread its output
+// offsets; pass 0 places the non-baseline tokens (budget < T), pass 1 the
+// baseline tokens (budget T) after all of them.
+constexpr int kPlanThreads = 1024, kPlanPer = 16;
+
+__global__ __launch_bounds__(kPlanThreads) void reorder_plan_kernel(const int32_t* __restrict__ budget,
+                                                                    int n, int T,
+                                                                    int32_t* __restrict__ perm,
+                                                                    int32_t* __restrict__ n_lead) {
+  __shared__ int wave_total[kPlanThreads / kWave];
+  __shared__ int bad_any;
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  if (t == 0) bad_any = 0;
+  __syncthreads();
+  int bad = 0, base = 0, lead_total = 0;
+  for (int pass = 0; pass < 2; ++pass) {
+    base = pass == 0 ? 0 : lead_total;
+    for (int c0 = 0; c0 < n; c0 += kPlanThreads * kPlanPer) {
+      const int e0 = c0 + t * kPlanPer;
+      unsigned mask = 0;
+#pragma unroll
+      for (int r = 0; r < kPlanPer; ++r) {
+        if (e0 + r < n) {
+          const int s = budget[e0 + r];
+          const bool ok = s >= 1 && s <= T && T % s == 0;
+          bad |= !ok;
+          const bool pick = pass == 0 ? (ok && s < T) : (!ok || s == T);
+          mask |= (pick ? 1u : 0u) << r;
+        }
+      }
+      const int cnt = __popc(mask);
+      int inc = cnt;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(inc, o);
+        if (lane >= o) inc += y;
+      }
+      if (lane == kWave - 1) wave_total[w] = inc;
+      __syncthreads();
+      int before = 0, total = 0;
+#pragma unroll
+      for (int i = 0; i < kPlanThreads / kWave; ++i) {
+        const int v = wave_total[i];
+        before += (i < w) ? v : 0;
+        total += v;
+      }
+      int pos = base + before + inc - cnt;
+      while (mask) {
+        const int r = __builtin_ctz(mask);
+        perm[pos++] = e0 + r;
+        mask &= mask - 1;
+      }
+      base += total;
+      __syncthreads();  // wave_total is rewritten by the next chunk
+    }
+    if (pass == 0) lead_total = base;
+  }
+  if (bad) atomicOr(&bad_any, 1);
+  __syncthreads();
+  if (t == 0) n_lead[0] = bad_any ? -1 : lead_total;
+}
+
+// dst row i <- src row perm[i] (or the inverse), 16-, 4- or 1-byte units
+template <typename U>
+__global__ __launch_bounds__(kThreads) void permute_rows_kernel(const U* __restrict__ src,
+                                                                const int32_t* __restrict__ perm,
+                                                                long n_rows, long units, bool inverse,
+                                                                U* __restrict__ dst) {
+  const long total = n_rows * units;
+  for (long e = blockIdx.x * (long)kThreads + threadIdx.x; e < total; e += (long)gridDim.x * kThreads) {
+    const long i = e / units, u = e - i * units;
+    const long p = perm[i];
+    if (p < 0 || p >= n_rows) continue;
+    if (inverse)
+      dst[p * units + u] = src[e];
+    else
+      dst[e] = src[p * units + u];
+  }
+}
+
 // one wave per row, fp32 sum of squares
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void row_rms_scale(const void* __restrict__ x, int n_rows,
@@ -260,6 +345,35 @@ hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active
     else
       hipLaunchKernelGGL(gather_latent_scalar<false>, grid, dim3(kThreads), 0, s, x, idx,
                          n_active, n_tokens, channels, xa);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reorder_plan(const int32_t* budget, int n, int T, int32_t* perm,
+                               int32_t* n_lead, hipStream_t s) {
+  hipLaunchKernelGGL(reorder_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, budget, n, T, perm,
+                     n_lead);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_rows(const void* src, const int32_t* perm, long n_rows, long row_bytes,
+                               bool inverse, void* dst, hipStream_t s) {
+  if (n_rows <= 0 || row_bytes <= 0) return hipSuccess;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst);
+  if (row_bytes % 16 == 0 && a % 16 == 0) {
+    const long u = row_bytes / 16;
+    hipLaunchKernelGGL(permute_rows_kernel<u32x4>, dim3(grid_for(n_rows * u)), dim3(kThreads), 0, s,
+                       static_cast<const u32x4*>(src), perm, n_rows, u, inverse,
+                       static_cast<u32x4*>(dst));
+  } else if (row_bytes % 4 == 0 && a % 4 == 0) {
+    const long u = row_bytes / 4;
+    hipLaunchKernelGGL(permute_rows_kernel<uint32_t>, dim3(grid_for(n_rows * u)), dim3(kThreads), 0,
+                       s, static_cast<const uint32_t*>(src), perm, n_rows, u, inverse,
+                       static_cast<uint32_t*>(dst));
+  } else {
+    hipLaunchKernelGGL(permute_rows_kernel<uint8_t>, dim3(grid_for(n_rows * row_bytes)),
+                       dim3(kThreads), 0, s, static_cast<const uint8_t*>(src), perm, n_rows,
+                       row_bytes, inverse, static_cast<uint8_t*>(dst));
   }
   return hipGetLastError();
 }

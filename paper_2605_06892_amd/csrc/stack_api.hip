@@ -211,6 +211,42 @@ HSA_API int hsa_rope_table(float theta, int32_t head_dim, int32_t grid_f, int32_
   return HSA_STEP_OK;
 }
 
+HSA_API int hsa_reorder_plan(const int32_t* budget, int64_t n_tokens, int32_t T, int32_t* perm,
+                             int32_t* n_lead_dev, int32_t* n_lead_host, hipStream_t stream) {
+  if (n_tokens < 0 || n_tokens > kMaxRows) return HSA_STEP_ERR_SHAPE;
+  if (T < 1) return HSA_STEP_ERR_BUDGET;
+  if (!n_lead_dev || (n_tokens > 0 && (!budget || !perm))) return HSA_STEP_ERR_NULL;
+  if (!aligned(budget, 4) || !aligned(perm, 4) || !aligned(n_lead_dev, 4)) return HSA_STEP_ERR_SHAPE;
+  const size_t nb = (size_t)n_tokens * 4;
+  if (overlaps(perm, nb, budget, nb) || overlaps(n_lead_dev, 4, budget, nb) ||
+      overlaps(n_lead_dev, 4, perm, nb))
+    return HSA_STEP_ERR_ALIAS;
+  if (hsa::launch_reorder_plan(budget, (int)n_tokens, T, perm, n_lead_dev, stream) != hipSuccess)
+    return HSA_STEP_ERR_LAUNCH;
+  if (n_lead_host) {
+    int32_t v = 0;
+    if (hipMemcpyAsync(&v, n_lead_dev, 4, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+    *n_lead_host = v;
+    if (v < 0) return HSA_STEP_ERR_BUDGET;
+  }
+  return HSA_STEP_OK;
+}
+
+HSA_API int hsa_permute_rows(const void* src, const int32_t* perm, int64_t n_rows, int64_t row_bytes,
+                             int32_t inverse, void* dst, hipStream_t stream) {
+  if (n_rows < 0 || n_rows > kMaxRows || row_bytes < 0) return HSA_STEP_ERR_SHAPE;
+  if (n_rows == 0 || row_bytes == 0) return HSA_STEP_OK;
+  if (!src || !perm || !dst) return HSA_STEP_ERR_NULL;
+  if (!aligned(perm, 4)) return HSA_STEP_ERR_SHAPE;
+  const size_t b = (size_t)n_rows * row_bytes;
+  if (overlaps(src, b, dst, b) || overlaps(perm, (size_t)n_rows * 4, dst, b))
+    return HSA_STEP_ERR_ALIAS;
+  return launch_status(hsa::launch_permute_rows(src, perm, n_rows, row_bytes, inverse != 0, dst,
+                                                stream));
+}
+
 HSA_API int hsa_l1_rel_accumulate(const float* v, float* v_prev, int64_t n_tokens,
                                   int32_t channels, double* acc, int32_t first,
                                   hipStream_t stream) {
@@ -254,6 +290,12 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       Lc < 0 || Lc > kMaxRows)
     return HSA_STEP_ERR_SHAPE;
   const bool rope = s->rope_cs != nullptr;
+  const bool prefix = s->prefix_cache != 0;
+  if (s->reserved3 != 0 || (s->prefix_cache != 0 && s->prefix_cache != 1)) return HSA_STEP_ERR_SHAPE;
+  if (prefix && (s->n_cached < 0 || s->n_cached > N)) return HSA_STEP_ERR_SHAPE;
+  if (prefix && n_groups != 0) return HSA_STEP_ERR_BUDGET;
+  const int64_t n_rows_cache = prefix ? s->n_cached : N;  // rows of each layer's cache
+  const int64_t n_tail = N - n_rows_cache;
   if (rope && (s->grid_f < 1 || s->grid_h < 1 || s->grid_w < 1 ||
                (int64_t)s->grid_f * s->grid_h * s->grid_w < N ||
                (int64_t)s->grid_f * s->grid_h * s->grid_w > kMaxRows))
@@ -274,7 +316,8 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   }
   if (!s->w_embed || !s->w_head || !s->x || !s->v_hat || !s->budget || !s->idx || !s->n_active ||
       !s->xa || !s->h || !s->q || !s->o || !s->v_fresh || !s->row_scale ||
-      (n_groups && !s->keys) || (l1rel && !s->v_prev) || (F > 0 && !s->f))
+      (n_groups && !s->keys) || (l1rel && !s->v_prev) || (F > 0 && !s->f) ||
+      (n_tail > 0 && (!s->k_tail || !s->v_tail)))
     return HSA_STEP_ERR_NULL;
   if (L > 0 && (!s->w_layers || !s->caches || (Lc > 0 && !s->w_cross) || (F > 0 && !s->w_ffn)))
     return HSA_STEP_ERR_NULL;
@@ -292,7 +335,11 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   if (n_groups) written.push_back({s->keys, (size_t)N * 8});
   if (l1rel) written.push_back({s->v_prev, (size_t)N * C * 4});
   if (F > 0) written.push_back({s->f, (size_t)N * F * es});
-  for (int i = 0; i < 2 * L; ++i) written.push_back({s->caches[i], (size_t)N * row_d});
+  if (n_tail > 0) {
+    written.push_back({s->k_tail, (size_t)n_tail * row_d});
+    written.push_back({s->v_tail, (size_t)n_tail * row_d});
+  }
+  for (int i = 0; i < 2 * L; ++i) written.push_back({s->caches[i], (size_t)n_rows_cache * row_d});
   std::vector<Span> weights = {{s->w_embed, (size_t)d * row_c}, {s->w_head, (size_t)C * row_d}};
   for (int i = 0; i < 4 * L; ++i) weights.push_back({s->w_layers[i], (size_t)d * row_d});
   for (int l = 0; l < L && Lc > 0; ++l) {
@@ -324,6 +371,13 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       hipStreamSynchronize(stream) != hipSuccess)
     return HSA_STEP_ERR_LAUNCH;
   if (n < 0 || n > N) return HSA_STEP_ERR_BUDGET;
+  if (n_tail > 0) {  // the baseline suffix must be active: the last n_tail entries of idx are it
+    if (n < n_tail) return HSA_STEP_ERR_BUDGET;
+    int32_t first = -1;
+    if (hipMemcpy(&first, s->idx + (n - n_tail), 4, hipMemcpyDeviceToHost) != hipSuccess)
+      return HSA_STEP_ERR_LAUNCH;
+    if (first != n_rows_cache) return HSA_STEP_ERR_BUDGET;
+  }
   if (n_active_host) *n_active_host = n;
   if (refreshed_host) *refreshed_host = 0;
 
@@ -333,9 +387,12 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   const float scale = 1.0f / sqrtf((float)dh);
   auto ok = [](hipError_t e) { return e == hipSuccess; };
   auto rms = [&]() { return ok(hsa::launch_row_rms_scale(s->h, bf, n, d, kRmsEps, s->row_scale, stream)); };
-  auto attend = [&](const void* q, const void* k, const void* v, int n_kv) {
-    return ok(bf ? hsa::launch_attention_bf16(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream)
-                 : hsa::launch_attention_f32(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream));
+  auto attend = [&](const void* q, const void* k, const void* v, int n_kv, const void* k2 = nullptr,
+                    const void* v2 = nullptr, int n_split = 0x7fffffff) {
+    return ok(bf ? hsa::launch_attention_bf16(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream,
+                                              k2, v2, n_split)
+                 : hsa::launch_attention_f32(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream, k2,
+                                             v2, n_split));
   };
   auto gemm = [&](const RowGemm& g) { return ok(launch_gemm(dt, g, stream)); };
   if (n > 0) {
@@ -358,6 +415,12 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
       g.out[0] = {w[0], s->q, nullptr, n};
       g.out[1] = {w[1], kc, s->idx, (int)N};
       g.out[2] = {w[2], vc, s->idx, (int)N};
+      if (n_tail > 0) {  // baseline rows: fresh keys and values only
+        g.out[1].C2 = s->k_tail;
+        g.out[1].c_split = (int)n_rows_cache;
+        g.out[2].C2 = s->v_tail;
+        g.out[2].c_split = (int)n_rows_cache;
+      }
       g.n_out = 3;
       g.row_scale = s->row_scale;
       if (rope) {
@@ -372,7 +435,10 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
         g.rope_h = s->grid_h;
         g.rope_w = s->grid_w;
       }
-      if (!rms() || !gemm(g) || !attend(s->q, kc, vc, (int)N) ||
+      const bool split = n_tail > 0;
+      if (!rms() || !gemm(g) ||
+          !attend(s->q, kc, vc, (int)N, split ? s->k_tail : nullptr, split ? s->v_tail : nullptr,
+                  split ? (int)n_rows_cache : 0x7fffffff) ||
           !gemm(compact_gemm(s->o, n, d, w[3], d, nullptr, s->h, false, s->h)))
         return HSA_STEP_ERR_LAUNCH;
       if (Lc > 0) {  // cross-attention of the active rows to the context

@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
             "hsa_linear": (ctypes.c_int, [ctypes.c_int, P, I32, I32, P, I32, P, P, I32, ctypes.c_int, P, P]),
             "hsa_l1_rel_accumulate": (ctypes.c_int, [P, P, I64, I32, P, I32, P]),
             "hsa_rope_table_floats": (S, [I32, I32, I32, I32]),
+            "hsa_reorder_plan": (ctypes.c_int, [P, I64, I32, P, P, P, P]),
+            "hsa_permute_rows": (ctypes.c_int, [P, P, I64, I64, I32, P, P]),
             "hsa_rope_table": (ctypes.c_int, [F, I32, I32, I32, I32, P]),
             "hsa_assign_budgets_by_key": (ctypes.c_int, [P, I64, I32, P, P, I32, P, P]),
             "hsa_assign_budgets_workspace_bytes": (S, [I64]),
@@ -98,6 +100,8 @@ EXPORTED = (
     "hsa_assign_budgets_by_key",
     "hsa_rope_table_floats",
     "hsa_rope_table",
+    "hsa_reorder_plan",
+    "hsa_permute_rows",
     "hsa_stack_iteration",
 )
 
@@ -124,6 +128,8 @@ class HsaStack(ctypes.Structure):
         ("rope_cs", ctypes.c_void_p), ("pos", ctypes.c_void_p),
         ("grid_f", ctypes.c_int32), ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32),
         ("reserved2", ctypes.c_int32),
+        ("prefix_cache", ctypes.c_int32), ("reserved3", ctypes.c_int32), ("n_cached", ctypes.c_int64),
+        ("k_tail", ctypes.c_void_p), ("v_tail", ctypes.c_void_p),
     ]
 
 
@@ -308,6 +314,29 @@ def hsa_assign_budgets_by_key(keys, T: int, group_sizes, budget, stream=None) ->
     _check("hsa_assign_budgets_by_key", st)
 
 
+def hsa_reorder_plan(budget, T: int, perm, n_lead_dev, stream=None) -> int:
+    """perm = non-baseline tokens then the budget-T group; returns their split
+    (one stream synchronization)."""
+    _dev(budget, perm, n_lead_dev)
+    host = ctypes.c_int32(-2)
+    st = lib().hsa_reorder_plan(_ptr(budget), budget.numel(), T, _ptr(perm), _ptr(n_lead_dev), ctypes.byref(host),
+                                _stream(stream))
+    _check("hsa_reorder_plan", st)
+    return host.value
+
+
+def hsa_permute_rows(src, perm, dst, inverse: bool = False, stream=None) -> None:
+    """dst[i] = src[perm[i]] (inverse: dst[perm[i]] = src[i]) over the rows of
+    src (first dimension)."""
+    _dev(src, perm, dst)
+    if src.dtype != dst.dtype or src.shape != dst.shape:
+        raise TypeError("src and dst must match")
+    n = src.shape[0]
+    row_bytes = src.numel() // max(n, 1) * src.element_size()
+    st = lib().hsa_permute_rows(_ptr(src), _ptr(perm), n, row_bytes, int(inverse), _ptr(dst), _stream(stream))
+    _check("hsa_permute_rows", st)
+
+
 def hsa_rope_table(theta: float, head_dim: int, grid) -> torch.Tensor:
     """The (cos, sin) table of the stack's rotary embedding, on the host
     (float32 [(F + H + W), head_dim])."""
@@ -321,14 +350,15 @@ def hsa_rope_table(theta: float, head_dim: int, grid) -> torch.Tensor:
 
 def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_active, xa, h, q, o, v_fresh,
                keys, row_scale, heads: int, head_dim: int, cross=None, ffn=None, f=None,
-               v_prev=None, rope_cs=None, pos=None, grid=(0, 0, 0)) -> HsaStack:
+               v_prev=None, rope_cs=None, pos=None, grid=(0, 0, 0), n_cached=None, k_tail=None,
+               v_tail=None) -> HsaStack:
     """Fill a struct hsa_stack from device tensors. layers: per layer
     (wq, wk, wv, wo); caches: per layer (k_hat, v_hat); cross: per layer
     (wq_c, wo_c, k_c, v_c) or None; ffn: per layer (w1, w2) or None. The
     returned struct keeps its host pointer arrays alive; the tensors must
     outlive it."""
     ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale, f, v_prev,
-          rope_cs, pos]
+          rope_cs, pos, k_tail, v_tail]
     ts += [t for lw in layers for t in lw] + [t for c in caches for t in c]
     ts += [t for lw in (cross or ()) for t in lw] + [t for lw in (ffn or ()) for t in lw]
     _dev(*ts)
@@ -348,7 +378,10 @@ def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_acti
                  ctx_len=0 if not cross else cross[0][2].shape[0],
                  f=0 if f is None else f.data_ptr(), v_prev=0 if v_prev is None else v_prev.data_ptr(),
                  rope_cs=0 if rope_cs is None else rope_cs.data_ptr(), pos=0 if pos is None else pos.data_ptr(),
-                 grid_f=grid[0], grid_h=grid[1], grid_w=grid[2], reserved2=0)
+                 grid_f=grid[0], grid_h=grid[1], grid_w=grid[2], reserved2=0,
+                 prefix_cache=0 if n_cached is None else 1, reserved3=0,
+                 n_cached=0 if n_cached is None else int(n_cached),
+                 k_tail=0 if k_tail is None else k_tail.data_ptr(), v_tail=0 if v_tail is None else v_tail.data_ptr())
     keep = [wl, cl]
     if cross:
         xl = (ctypes.c_void_p * (4 * len(cross)))(*[t.data_ptr() for lw in cross for t in lw])

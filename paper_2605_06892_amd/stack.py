@@ -45,6 +45,9 @@ class StackBuffers:
     rope_cs: torch.Tensor | None = None  # rotary (cos, sin) table on the device
     pos: torch.Tensor | None = None      # int32 [N] grid position of every token
     grid: tuple = (0, 0, 0)
+    n_cached: int | None = None          # prefix-only cache: rows per layer cache
+    k_tail: torch.Tensor | None = None   # [N - n_cached, d] fresh baseline keys
+    v_tail: torch.Tensor | None = None
     _handle: H.HsaStack | None = field(default=None, repr=False)
 
     @property
@@ -61,17 +64,23 @@ class StackBuffers:
 
     @classmethod
     def allocate(cls, N: int, C: int, n_layers: int, heads: int, head_dim: int, dtype: torch.dtype,
-                 device="cuda", ffn: int = 0, ctx: int = 0) -> "StackBuffers":
+                 device="cuda", ffn: int = 0, ctx: int = 0, n_cached: int | None = None) -> "StackBuffers":
         """Tensors for N tokens, C latent values per token, n_layers layers of
         width heads * head_dim; ffn > 0 / ctx > 0 add the FFN and
-        cross-attention sub-layers of full blocks."""
+        cross-attention sub-layers of full blocks; n_cached (prefix-only
+        cache of reordered tokens, Section 2.5) sizes each layer's cache to
+        the non-baseline prefix."""
         d = heads * head_dim
         e = lambda *s, dt=dtype: torch.empty(*s, dtype=dt, device=device)  # noqa: E731
         f32 = torch.float32
+        rows = N if n_cached is None else n_cached
+        tail = None if n_cached is None else N - n_cached
         return cls(x=e(N, C, dt=f32), v_hat=e(N, C, dt=f32), budget=e(N, dt=torch.int32),
                    w_embed=e(d, C), w_head=e(C, d),
                    layers=[tuple(e(d, d) for _ in range(4)) for _ in range(n_layers)],
-                   caches=[(e(N, d), e(N, d)) for _ in range(n_layers)],
+                   caches=[(e(max(rows, 1), d), e(max(rows, 1), d)) for _ in range(n_layers)],
+                   n_cached=n_cached, k_tail=None if tail is None else e(max(tail, 1), d),
+                   v_tail=None if tail is None else e(max(tail, 1), d),
                    idx=e(N, dt=torch.int32), n_active=e(1, dt=torch.int32), xa=e(N, C), h=e(N, d), q=e(N, d),
                    o=e(N, d), v_fresh=e(N, C, dt=f32), keys=e(N, dt=torch.float64), row_scale=e(N, dt=f32),
                    v_prev=e(N, C, dt=f32), heads=heads, head_dim=head_dim,
@@ -104,8 +113,36 @@ class StackBuffers:
                                         v_fresh=self.v_fresh, keys=self.keys, row_scale=self.row_scale,
                                         heads=self.heads, head_dim=self.head_dim, cross=self.cross,
                                         ffn=self.ffn, f=self.f, v_prev=self.v_prev, rope_cs=self.rope_cs,
-                                        pos=self.pos, grid=self.grid)
+                                        pos=self.pos, grid=self.grid, n_cached=self.n_cached,
+                                        k_tail=self.k_tail, v_tail=self.v_tail)
         return self._handle
+
+
+def reorder(b: StackBuffers, T: int) -> torch.Tensor:
+    """Token reordering before the loop (Section 2.5): non-baseline tokens
+    first, the budget-T group last. Permutes the latent, the velocity cache,
+    the budgets and the grid positions (created if absent) on the device and
+    returns the permutation (new position i holds old token perm[i])."""
+    perm = torch.empty(b.N, dtype=torch.int32, device=b.x.device)
+    n_lead = torch.empty(1, dtype=torch.int32, device=b.x.device)
+    lead = H.hsa_reorder_plan(b.budget, T, perm, n_lead)
+    if b.n_cached is not None and lead != b.n_cached:
+        raise ValueError(f"{lead} non-baseline tokens but caches sized for {b.n_cached}")
+    if b.pos is None:
+        b.pos = torch.arange(b.N, dtype=torch.int32, device=b.x.device)
+    for t in (b.x, b.v_hat, b.budget, b.pos):
+        tmp = torch.empty_like(t)
+        H.hsa_permute_rows(t, perm, tmp)
+        t.copy_(tmp)
+    b._handle = None
+    return perm
+
+
+def restore_order(b: StackBuffers, perm: torch.Tensor) -> torch.Tensor:
+    """The latent in the original token order (the reordering inverted)."""
+    out = torch.empty_like(b.x)
+    H.hsa_permute_rows(b.x, perm, out, inverse=True)
+    return out
 
 
 def iteration(b: StackBuffers, T: int, i: int, sigmas, group_sizes=None, margin: int = 0,

@@ -335,3 +335,33 @@ def test_rope_table_matches_the_oracle_angles(lib):
     assert lib.hsa_rope_table_floats(128, 0, 30, 52) == 0
     assert lib.hsa_rope_table(10000.0, 128, 2, 2, 2, None) == NULL
     assert lib.hsa_rope_table(0.5, 128, 2, 2, 2, A) == SHAPE
+
+
+def test_reorder_and_permute_errors(lib):
+    f = lib.hsa_reorder_plan
+    assert f(A, -1, 40, B, C, None, None) == SHAPE
+    assert f(A, 100, 0, B, C, None, None) == BUDGET
+    assert f(None, 100, 40, B, C, None, None) == NULL
+    assert f(A, 100, 40, B, None, None, None) == NULL
+    assert f(A, 100, 40, A + 8, C, None, None) == ALIAS       # perm inside budget
+    assert f(A, 100, 40, B, B + 16, None, None) == ALIAS      # count inside perm
+    g = lib.hsa_permute_rows
+    assert g(A, B, -1, 64, 0, C, None) == SHAPE
+    assert g(None, B, 10, 64, 0, C, None) == NULL
+    assert g(A, B, 10, 64, 0, A + 32, None) == ALIAS          # dst over src
+    assert g(A, B, 10, 64, 0, B, None) == ALIAS               # dst over perm
+    assert g(A, B + 2, 10, 64, 0, C, None) == SHAPE           # misaligned perm
+    assert g(None, None, 0, 64, 0, None, None) == OK
+
+
+def test_prefix_cache_stack_errors(lib):
+    f = lib.hsa_stack_iteration
+    gb = (ctypes.c_int32 * 2)(20, 40)
+    gs = (ctypes.c_int64 * 2)(500, 500)
+    call = lambda s, g=0: f(ctypes.byref(s), 40, 1, 0, 1, 1.0, 0.975, gb, gs, g, 0, None, None, None)  # noqa: E731
+    assert call(_stack(prefix_cache=1, n_cached=500)[0], g=2) == BUDGET   # fixed groups only
+    assert call(_stack(prefix_cache=1, n_cached=1001)[0]) == SHAPE
+    assert call(_stack(prefix_cache=1, n_cached=-1)[0]) == SHAPE
+    assert call(_stack(prefix_cache=2, n_cached=500)[0]) == SHAPE
+    assert call(_stack(prefix_cache=1, n_cached=500)[0]) == NULL         # tails missing
+    assert call(_stack(reserved3=1)[0]) == SHAPE

@@ -383,3 +383,127 @@ def test_wan13b_full_blocks_iterations():
     for (k, v), (k0, v0_) in zip(b.caches, before):
         assert torch.equal(k[skipped], k0[skipped]) and torch.equal(v[skipped], v0_[skipped])
     assert torch.isfinite(b.v_fresh[:n]).all()
+
+
+# ---------------------------------------------------------------------------
+# Token reordering and the prefix-only cache (Section 2.5)
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("N,bad", [(1000, False), (75600, False), (37, False), (5000, True)])
+def test_reorder_plan(N, bad):
+    rng = np.random.default_rng(N)
+    b = rng.choice(np.array([40, 20, 10, 5]), size=N).astype(np.int32)
+    if bad:
+        b[77] = 3
+    perm = torch.full((N,), -1, dtype=torch.int32, device=DEV)
+    n_lead = torch.zeros(1, dtype=torch.int32, device=DEV)
+    if bad:
+        with pytest.raises(H.HsaStepError) as e:
+            H.hsa_reorder_plan(i32(b), 40, perm, n_lead)
+        assert e.value.name == "HSA_STEP_ERR_BUDGET"
+        assert sorted(perm.cpu().numpy().tolist()) == list(range(N))  # still a permutation
+        return
+    lead = H.hsa_reorder_plan(i32(b), 40, perm, n_lead)
+    want, want_lead = oracle.reorder_plan(b, 40)
+    assert lead == want_lead
+    np.testing.assert_array_equal(perm.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("shape,dtype", [((1000, 64), torch.float32), ((777, 3), torch.float32),
+                                          ((500,), torch.int32), ((300, 5), torch.bfloat16),
+                                          ((32760, 1536), torch.bfloat16)])
+def test_permute_rows(shape, dtype):
+    n = shape[0]
+    src = torch.randn(*shape, device=DEV).to(dtype) if dtype != torch.int32 else \
+        torch.randint(-99, 99, shape, dtype=torch.int32, device=DEV)
+    perm_np = np.random.default_rng(n).permutation(n).astype(np.int32)
+    perm = i32(perm_np)
+    dst = torch.empty_like(src)
+    H.hsa_permute_rows(src, perm, dst)
+    assert torch.equal(dst, src[torch.from_numpy(perm_np).long().to(DEV)])
+    back = torch.empty_like(src)
+    H.hsa_permute_rows(dst, perm, back, inverse=True)
+    assert torch.equal(back, src)
+
+
+def test_tiny_prefix_cache_trajectory():
+    """Reordered tokens with the prefix-only cache and RoPE by original grid
+    positions: the GPU trajectory matches the oracle's reordered trajectory,
+    and the restored latent matches the oracle's unreordered one."""
+    wl = synth.WORKLOADS["tiny_block_f32"]
+    wts = synth.draw_stack(wl, seed=61)
+    budget = synth.assign_budgets(np.zeros((wl.N, 1), np.float32), wl.groups, "first_frame",
+                                  frame_tokens=wl.grid[1] * wl.grid[2], seed=62)
+    sig = synth.linear_sigmas(wl.T)
+    perm_o, n_cached = oracle.reorder_plan(budget, wl.T)
+    st1 = oracle.initial_state(wts["x0"][perm_o], wl.layers, wl.d, wl.T)
+    st1["budget"] = budget[perm_o]
+    recs = oracle.stack_trajectory(None, wts, wl.T, sig, wl.heads, wl.dh, "f32", state=st1,
+                                   rope={"grid": wl.grid, "pos": perm_o})
+    b = S.StackBuffers.allocate(wl.N, wl.euler_channels, wl.layers, wl.heads, wl.dh, torch.float32,
+                                ffn=wl.ffn, ctx=wl.ctx, n_cached=n_cached)
+    src = _upload(wl, wts, wl.N, wl.layers)  # weights and context, full-cache layout
+    for name in ("w_embed", "w_head"):
+        getattr(b, name).copy_(getattr(src, name))
+    for dst, s_ in zip(b.layers + b.cross + b.ffn, src.layers + src.cross + src.ffn):
+        for a, c in zip(dst, s_):
+            a.copy_(c)
+    b.x.copy_(to_dev(wts["x0"], "f32"))
+    b.v_hat.zero_()
+    b.budget.copy_(i32(budget))
+    b.enable_rope(wl.grid)
+    perm = S.reorder(b, wl.T)
+    np.testing.assert_array_equal(perm.cpu().numpy(), perm_o)
+    for r in recs:
+        n, _ = S.iteration(b, wl.T, r["i"], sig)
+        assert n == r["idx"].size
+        np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), r["idx"])
+        assert rel_inf(host(b.x), r["x"]) <= TOL["f32"], r["i"]
+        for (k, v), (kr, vr) in zip(b.caches, r["caches"]):
+            assert rel_inf(host(k[:n_cached]), kr[:n_cached]) <= TOL["f32"], r["i"]
+            assert rel_inf(host(v[:n_cached]), vr[:n_cached]) <= TOL["f32"], r["i"]
+    st0 = oracle.initial_state(wts["x0"], wl.layers, wl.d, wl.T)
+    st0["budget"] = budget
+    base = oracle.stack_trajectory(None, wts, wl.T, sig, wl.heads, wl.dh, "f32", state=st0,
+                                   rope={"grid": wl.grid, "pos": None})
+    assert rel_inf(host(S.restore_order(b, perm)), base[-1]["x"]) <= TOL["f32"]
+
+
+def test_prefix_cache_equals_full_cache_bitwise():
+    """At the Wan-1.3B shape (3 layers, RoPE, HSA-75A groups with a 25%
+    baseline group reordered to the end) the prefix-only cache changes only
+    where the baseline rows' keys live: latents, velocities and the cached
+    prefix rows are bit-identical to the full-cache run."""
+    wl = synth.WORKLOADS["wan1.3b_stack"]
+    N, L = wl.N, 3
+    wts = synth.draw_stack(wl, seed=7, layers=L)
+    groups = synth.PRESETS["HSA-75A"]["groups"]
+    budget = synth.random_budgets(N, groups, seed=8)
+    sig = synth.linear_sigmas(wl.T)
+    runs = []
+    for n_cached in (None, int(np.sum(budget < wl.T))):
+        b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch.bfloat16, n_cached=n_cached)
+        src = _upload(wl, wts, N, L) if not runs else runs[0][0]
+        if runs:
+            for name in ("w_embed", "w_head"):
+                getattr(b, name).copy_(getattr(src, name))
+            for dst, s_ in zip(b.layers, src.layers):
+                for a, c in zip(dst, s_):
+                    a.copy_(c)
+        else:
+            b = src
+        b.x.copy_(to_dev(wts["x0"], "f32"))
+        b.v_hat.zero_()
+        b.budget.copy_(i32(budget))
+        b.pos = None
+        b.enable_rope(wl.grid)
+        S.reorder(b, wl.T)
+        for i in range(3):  # 100%, then the 40+20 groups, then 40 only
+            S.iteration(b, wl.T, i, sig)
+        runs.append((b, n_cached))
+    (full, _), (pre, n_cached) = runs
+    assert torch.equal(full.x, pre.x) and torch.equal(full.v_hat, pre.v_hat)
+    for (k0, v0), (k1, v1) in zip(full.caches, pre.caches):
+        assert torch.equal(k0[:n_cached], k1) and torch.equal(v0[:n_cached], v1)
+    assert torch.equal(full.caches[-1][0][n_cached:], pre.k_tail)  # the last layer's fresh baseline keys
