@@ -345,7 +345,7 @@ def stack_flops(n_active, N, d, C, layers, ffn=0, ctx=0):
     return 2.0 * n_active * C * d * 2 + layers * per_layer
 
 
-def end_to_end(dev, name="wan1.3b_stack", presets=False):
+def end_to_end(dev, name="wan1.3b_stack", presets=False, rope=False):
     """Whole T = 40 sampling loops of a 30-layer Wan-1.3B-shaped stack on the
     same seed and weights: the dense loop (every token at every iteration:
     flow matching with T = 40) and the HSA loop with budgets {40, 20, 10, 5}
@@ -384,35 +384,44 @@ def end_to_end(dev, name="wan1.3b_stack", presets=False):
         for dst, lw in zip(b.ffn, wts["layers"]):
             dst[0].copy_(bf(lw["w1"]))
             dst[1].copy_(bf(lw["w2"]))
+    if rope:
+        b.enable_rope(wl.grid)
     x0 = torch.from_numpy(wts["x0"]).to(dev)
     del wts
     t_draw = time.perf_counter() - t_draw
     sig = synth.linear_sigmas(T)
 
-    def loop(groups, budget0=None, margin=0, outside_period=1, selection=H.SELECT_VELOCITY_NORM, iterations=T):
-        b.x.copy_(x0)
-        b.v_hat.zero_()
+    def loop(groups, budget0=None, margin=0, outside_period=1, selection=H.SELECT_VELOCITY_NORM, iterations=T,
+             bufs=None, reorder=False):
+        bb = b if bufs is None else bufs
+        bb.x.copy_(x0)
+        bb.v_hat.zero_()
         if budget0 is None:
-            b.budget.fill_(T)
+            bb.budget.fill_(T)
         else:
-            b.budget.copy_(torch.from_numpy(budget0))
+            bb.budget.copy_(torch.from_numpy(budget0))
+        if reorder:
+            if bb.pos is not None:
+                bb.pos.copy_(torch.arange(N, dtype=torch.int32, device=dev))
+            S.reorder(bb, T)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        res = S.run(b, T, sig, groups, margin=margin, iterations=iterations, outside_period=outside_period,
+        res = S.run(bb, T, sig, groups, margin=margin, iterations=iterations, outside_period=outside_period,
                     selection=selection)
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3
         fl = sum(stack_flops(n, N, d, C, L, wl.ffn, wl.ctx) for n, _ in res)
         return ms, {"token_step_fraction": round(sum(n for n, _ in res) / (N * T), 4),
                     "refreshes": int(sum(r for _, r in res)), "tflops": round(fl / (ms * 1e-3) / 1e12, 1),
-                    "final_latent_finite": bool(torch.isfinite(b.x).all())}
+                    "final_latent_finite": bool(torch.isfinite(bb.x).all())}
 
     sizes = synth.group_sizes(N, wl.groups)
     loop(sizes, iterations=2)  # warm-up: a dense and a partial iteration
     dense_ms, dense = loop(None)
     hsa_ms, hsa = loop(sizes)
     out = {
-        "workload": (f"{name}: {L} {'full blocks (FFN ' + str(wl.ffn) + ', context ' + str(wl.ctx) + ')' if wl.ffn else 'layers'}, "
+        "workload": (f"{name}: {L} {'full blocks (FFN ' + str(wl.ffn) + ', context ' + str(wl.ctx) + ')' if wl.ffn else 'layers'}"
+                     f"{', 3D RoPE by token position' if rope else ''}, "
                      f"N={N} ({'x'.join(map(str, wl.grid))}), d={d} ({wl.heads}x{wl.dh}), C={C} fp32 latent, bf16 model, "
                      f"T={T}, budgets {{40,20,10,5}} on quarters by velocity-norm rank, refreshed every "
                      f"{math.lcm(*[T // s for s, _ in sizes])} iterations"),
@@ -445,6 +454,32 @@ def end_to_end(dev, name="wan1.3b_stack", presets=False):
                 ms, r2 = loop(None, budget0=budget0, margin=m, outside_period=T // s_max)
                 r2.update({"ms": round(ms, 1), "runtime_vs_dense": round(ms / dense_ms, 4)})
                 out[pname]["outside_period_T_over_smax"] = r2
+        # token reordering + prefix-only cache (Section 2.5): HSA-75A groups with the first
+        # frame reserved for the baseline group (strategy F), same loop with full and prefix caches
+        pre = synth.PRESETS["HSA-75A"]
+        budget0 = synth.assign_budgets(np.zeros((N, 1), np.float32), pre["groups"], "first_frame",
+                                       frame_tokens=wl.grid[1] * wl.grid[2], seed=0)
+        m = LY.window_margin(pre["window"], T)
+        n_cached = S.prefix_rows(int(np.sum(budget0 < T)), N)
+        pb = S.StackBuffers.allocate(N, C, L, wl.heads, wl.dh, torch.bfloat16, device=dev, ffn=wl.ffn,
+                                     ctx=wl.ctx, n_cached=n_cached)
+        for f in ("w_embed", "w_head", "layers", "cross", "ffn", "rope_cs", "grid"):
+            setattr(pb, f, getattr(b, f))  # the same weights and tables
+        if pb.rope_cs is not None:
+            pb.pos = torch.arange(N, dtype=torch.int32, device=dev)
+        full_ms, rf = loop(None, budget0=budget0, margin=m, reorder=True)
+        full_x = b.x.clone()
+        pre_ms, rp = loop(None, budget0=budget0, margin=m, bufs=pb, reorder=True)
+        es = 2
+        out["reordered_prefix_cache"] = {
+            "groups": "HSA-75A, first frame reserved (strategy F), reordered once before the loop",
+            "cache_bytes_full": 2 * L * N * d * es, "cache_bytes_prefix": 2 * L * n_cached * d * es,
+            "tail_bytes": 2 * (N - n_cached) * d * es,
+            "full_cache_ms": round(full_ms, 1), "prefix_cache_ms": round(pre_ms, 1),
+            "runtime_vs_dense": round(pre_ms / dense_ms, 4), "token_step_fraction": rp["token_step_fraction"],
+            "latents_bit_identical": bool(torch.equal(full_x, pb.x)),
+        }
+        del pb
     return out
 
 
@@ -509,7 +544,7 @@ def main():
         out = {"end_to_end": end_to_end(dev)}
         if not args.no_blocks:
             torch.cuda.empty_cache()
-            out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True)
+            out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True, rope=True)
         print(json.dumps(out))
         return
     wl = synth.WORKLOADS[args.workload]
@@ -607,7 +642,7 @@ def main():
         out["end_to_end"] = end_to_end(dev)
         torch.cuda.empty_cache()
         if not args.no_blocks:
-            out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True)
+            out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True, rope=True)
             torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, blk, budget, args.iteration)

@@ -397,7 +397,9 @@ typedef struct hsa_stack {
                                      n_cached rows and the baseline rows' fresh keys and values
                                      live in k_tail/v_tail. Needs n_groups == 0 (fixed groups). */
   int32_t reserved3;              /* 0 */
-  int64_t n_cached;               /* 0 .. N (prefix_cache only) */
+  int64_t n_cached;               /* prefix_cache only: a multiple of 64, or N, at least the
+                                     number of non-baseline tokens (baseline tokens in the
+                                     prefix are cached and rewritten at every iteration) */
   void* k_tail;                   /* scratch [N - n_cached, d] dtype shared by the layers */
   void* v_tail;
 } hsa_stack;

@@ -15,8 +15,9 @@
 // heads; V: f(r) = (r&3)<<2), so that the K fragment reads (16 rows, one chunk)
 // and the V transpose reads (4 rows, 4 chunks) both hit disjoint LDS banks.
 // Rows beyond N are loaded from row N-1 and masked out of the softmax. The N
-// rows may come in two segments: a cache prefix and, from row n_split on,
-// fresh rows of a second buffer (the prefix-only cache of reordered tokens).
+// rows may come in two segments: a cache prefix and, from row n_split on (a
+// multiple of the 64-row tile), fresh rows of a second buffer (the
+// prefix-only cache of reordered tokens).
 //
 // Keys are consumed in 32-row blocks. Per block:
 //   S^T = K Q^T - m   v_mfma_f32_32x32x16_bf16 with K rows as the A operand
@@ -72,7 +73,7 @@ __device__ __forceinline__ int swz_v(int r) {
   return DH == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
 }
 
-template <int DH, int NW>
+template <int DH, int NW, bool SPLIT>
 __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
     bf16* __restrict__ o, int n_q, int n_kv, int d, float sl2e, int n_qtiles,
@@ -129,16 +130,20 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   auto issue_tile = [&](auto buf, int kv0) {
     bf16* kd = kbuf(buf);
     bf16* vd = vbuf(buf);
+    // segment of this tile (a tile never straddles the split: n_split is a
+    // multiple of BKV), chosen once per tile
+    const bool tail = SPLIT && kv0 >= n_split;
+    const bf16* kb = tail ? kg2 : kg;
+    const bf16* vb = tail ? vg2 : vg;
+    const long off = tail ? (long)n_split : 0;
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int seg = i * NW + wave;
       const int row = seg * RPS + lane / CPR;
       const int slot = lane % CPR;
-      const long n = min(kv0 + row, n_kv - 1);
-      const bool first = n < n_split;
-      const long r = first ? n : n - n_split;
-      const bf16* ks = (first ? kg : kg2) + r * d + (slot ^ swz_k<DH>(row)) * 8;
-      const bf16* vs = (first ? vg : vg2) + r * d + (slot ^ swz_v<DH>(row)) * 8;
+      const long n = min(kv0 + row, n_kv - 1) - off;
+      const bf16* ks = kb + n * d + (slot ^ swz_k<DH>(row)) * 8;
+      const bf16* vs = vb + n * d + (slot ^ swz_v<DH>(row)) * 8;
       __builtin_amdgcn_global_load_lds((global_cvoid*)ks, (lds_void*)(kd + seg * 512), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((global_cvoid*)vs, (lds_void*)(vd + seg * 512), 16, 0, 0);
     }
@@ -290,19 +295,31 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   }
 }
 
-template <int DH, int NW>
-hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
-                      int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
-                      int n_split) {
+template <int DH, int NW, bool SPLIT>
+hipError_t launch_split(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
+                        int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
+                        int n_split) {
   constexpr int BQ = NW * 32;
   const int n_qtiles = (n_q + BQ - 1) / BQ;
   const int d = heads * DH;
-  hipLaunchKernelGGL((attention_bf16_kernel<DH, NW>), dim3((unsigned)(n_qtiles * heads)),
+  hipLaunchKernelGGL((attention_bf16_kernel<DH, NW, SPLIT>), dim3((unsigned)(n_qtiles * heads)),
                      dim3(NW * 64), 0, s, static_cast<const bf16*>(q),
                      static_cast<const bf16*>(k), static_cast<const bf16*>(v),
                      static_cast<bf16*>(o), n_q, n_kv, d, sl2e, n_qtiles,
                      static_cast<const bf16*>(k2), static_cast<const bf16*>(v2), n_split);
   return hipGetLastError();
+}
+
+// keys in two segments only when the split falls inside the rows
+template <int DH, int NW>
+hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
+                      int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
+                      int n_split) {
+  if (n_split < n_kv) {
+    if (n_split % BKV != 0) return hipErrorInvalidValue;
+    return launch_split<DH, NW, true>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
+  }
+  return launch_split<DH, NW, false>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
 }
 
 }  // namespace

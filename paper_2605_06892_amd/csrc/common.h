@@ -140,7 +140,8 @@ __device__ __forceinline__ RowGemmOut row_gemm_out(const RowGemm& g, int z) {
 hipError_t launch_row_gemm_f32(const RowGemm& g, hipStream_t s);
 
 // Keys/values: rows n < n_split come from (k, v), rows n_split .. n_kv-1 from
-// (k2, v2) at row n - n_split (a cache prefix followed by fresh rows).
+// (k2, v2) at row n - n_split (a cache prefix followed by fresh rows). The
+// bf16 kernel needs n_split to be a multiple of 64 (its key tile).
 hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, void* o, int n_q,
                                  int n_kv, int heads, int head_dim, float scale, hipStream_t s,
                                  const void* k2 = nullptr, const void* v2 = nullptr,

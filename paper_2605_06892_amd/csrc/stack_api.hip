@@ -292,7 +292,8 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   const bool rope = s->rope_cs != nullptr;
   const bool prefix = s->prefix_cache != 0;
   if (s->reserved3 != 0 || (s->prefix_cache != 0 && s->prefix_cache != 1)) return HSA_STEP_ERR_SHAPE;
-  if (prefix && (s->n_cached < 0 || s->n_cached > N)) return HSA_STEP_ERR_SHAPE;
+  if (prefix && (s->n_cached < 0 || s->n_cached > N || (s->n_cached % 64 != 0 && s->n_cached != N)))
+    return HSA_STEP_ERR_SHAPE;
   if (prefix && n_groups != 0) return HSA_STEP_ERR_BUDGET;
   const int64_t n_rows_cache = prefix ? s->n_cached : N;  // rows of each layer's cache
   const int64_t n_tail = N - n_rows_cache;

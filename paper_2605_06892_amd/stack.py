@@ -126,7 +126,7 @@ def reorder(b: StackBuffers, T: int) -> torch.Tensor:
     perm = torch.empty(b.N, dtype=torch.int32, device=b.x.device)
     n_lead = torch.empty(1, dtype=torch.int32, device=b.x.device)
     lead = H.hsa_reorder_plan(b.budget, T, perm, n_lead)
-    if b.n_cached is not None and lead != b.n_cached:
+    if b.n_cached is not None and lead > b.n_cached:
         raise ValueError(f"{lead} non-baseline tokens but caches sized for {b.n_cached}")
     if b.pos is None:
         b.pos = torch.arange(b.N, dtype=torch.int32, device=b.x.device)
@@ -136,6 +136,12 @@ def reorder(b: StackBuffers, T: int) -> torch.Tensor:
         t.copy_(tmp)
     b._handle = None
     return perm
+
+
+def prefix_rows(n_lead: int, N: int) -> int:
+    """Cache rows of the prefix-only cache for n_lead non-baseline tokens: the
+    next multiple of the 64-row attention tile (at most N)."""
+    return min(N, -(-n_lead // 64) * 64)
 
 
 def restore_order(b: StackBuffers, perm: torch.Tensor) -> torch.Tensor:

@@ -359,9 +359,10 @@ def test_prefix_cache_stack_errors(lib):
     gb = (ctypes.c_int32 * 2)(20, 40)
     gs = (ctypes.c_int64 * 2)(500, 500)
     call = lambda s, g=0: f(ctypes.byref(s), 40, 1, 0, 1, 1.0, 0.975, gb, gs, g, 0, None, None, None)  # noqa: E731
-    assert call(_stack(prefix_cache=1, n_cached=500)[0], g=2) == BUDGET   # fixed groups only
+    assert call(_stack(prefix_cache=1, n_cached=512)[0], g=2) == BUDGET   # fixed groups only
     assert call(_stack(prefix_cache=1, n_cached=1001)[0]) == SHAPE
     assert call(_stack(prefix_cache=1, n_cached=-1)[0]) == SHAPE
-    assert call(_stack(prefix_cache=2, n_cached=500)[0]) == SHAPE
-    assert call(_stack(prefix_cache=1, n_cached=500)[0]) == NULL         # tails missing
+    assert call(_stack(prefix_cache=1, n_cached=500)[0]) == SHAPE        # not a multiple of the key tile
+    assert call(_stack(prefix_cache=2, n_cached=512)[0]) == SHAPE
+    assert call(_stack(prefix_cache=1, n_cached=512)[0]) == NULL         # tails missing
     assert call(_stack(reserved3=1)[0]) == SHAPE

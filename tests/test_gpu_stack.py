@@ -436,7 +436,8 @@ def test_tiny_prefix_cache_trajectory():
     budget = synth.assign_budgets(np.zeros((wl.N, 1), np.float32), wl.groups, "first_frame",
                                   frame_tokens=wl.grid[1] * wl.grid[2], seed=62)
     sig = synth.linear_sigmas(wl.T)
-    perm_o, n_cached = oracle.reorder_plan(budget, wl.T)
+    perm_o, n_lead = oracle.reorder_plan(budget, wl.T)
+    n_cached = S.prefix_rows(n_lead, wl.N)
     st1 = oracle.initial_state(wts["x0"][perm_o], wl.layers, wl.d, wl.T)
     st1["budget"] = budget[perm_o]
     recs = oracle.stack_trajectory(None, wts, wl.T, sig, wl.heads, wl.dh, "f32", state=st1,
@@ -482,7 +483,7 @@ def test_prefix_cache_equals_full_cache_bitwise():
     budget = synth.random_budgets(N, groups, seed=8)
     sig = synth.linear_sigmas(wl.T)
     runs = []
-    for n_cached in (None, int(np.sum(budget < wl.T))):
+    for n_cached in (None, S.prefix_rows(int(np.sum(budget < wl.T)), N)):
         b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch.bfloat16, n_cached=n_cached)
         src = _upload(wl, wts, N, L) if not runs else runs[0][0]
         if runs:
