@@ -8,16 +8,18 @@
 //     tokens fused into the epilogue.
 // The compact gathered activations are never materialized in HBM.
 //
-// Tiling: BM x BN output tile per 512-thread workgroup (8 waves in a WM x WN
-// grid), K step 64, v_mfma_f32_32x32x16_bf16; the fragments of the next
-// 16-wide k slice are read from LDS while the MFMAs of the current one run.
-// Tiles go global -> LDS directly
-// (global_load_lds_dwordx4: one wave instruction fills one contiguous 1 KB
-// segment = 8 tile rows of 128 bytes) into two stages, the loads of step k+1
-// in flight during the MFMAs of step k, one barrier per step. The 16-byte
-// chunks of tile row r sit at slot chunk ^ ((r >> 1) & 7), which keeps the
-// fragment reads (16 rows, one chunk) on disjoint banks. Each stage is its own
-// LDS array and the K loop is unrolled by 2, so the compiler can tell the
+// Tiling (struct Tiling): BM x BN output tile per workgroup of 8 waves in a
+// WM x WN grid, K step 64, v_mfma_f32_32x32x16_bf16. Tiles go global -> LDS
+// directly (global_load_lds_dwordx4: one wave instruction fills one
+// contiguous 1 KB segment = 8 tile rows of 128 bytes) into two stages, the
+// loads of step k+1 in flight during the MFMAs of step k, one barrier per
+// step. Within a step the fragment reads of k slice s+1 and the stage loads
+// are placed one per MFMA between the MFMAs of slice s, so neither the LDS
+// latency nor the load issue stalls the matrix pipe (measured: issuing them
+// in bursts ahead of the MFMAs cost 5-10%). The 16-byte chunks of tile row r
+// sit at slot chunk ^ ((r >> 1) & 7), which keeps the fragment reads (16
+// rows, one chunk) on disjoint banks. Each stage is its own LDS array and the
+// K loop is unrolled by the stage count, so the compiler can tell the
 // asynchronous loads from reads of the other stage.
 // Every tile row is a contiguous 128-byte run of a token row, so the indexed
 // loads stay coalesced; rows outside the problem are read from a valid row and
@@ -33,7 +35,6 @@
 namespace hsa {
 namespace {
 
-constexpr int BK = 64, kWaves = 8, kThreads = kWaves * 64;
 constexpr int kGroupM = 8;
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -41,28 +42,66 @@ typedef __attribute__((address_space(1))) const void global_cvoid;
 
 constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+// f(integral_constant<int, I>) for I = B .. E-1, unrolled at compile time
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // Epilogues (after the optional per-row scale): bf16 store, bf16 store of
 // (product + bf16 residual) rounded once, fp32 store, bf16 store of the tanh
 // GELU of the product.
 enum Epilogue { kEpiBf16 = 0, kEpiBf16Residual = 1, kEpiF32 = 2, kEpiBf16Gelu = 3 };
 
+// One tiling of the kernel: BM x BN output tile, K step BK (32 or 64),
+// STAGES LDS stages (loads run STAGES-1 steps ahead), WAVES waves in a
+// WM x (WAVES/WM) grid.
+template <int BM_, int BN_, int BK_, int STAGES_, int WAVES_, int WM_>
+struct Tiling {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_, WAVES = WAVES_, WM = WM_;
+  static constexpr int WN = WAVES / WM, THREADS = WAVES * 64;
+  static constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
+  static constexpr int MI = TM / 32, NI = TN / 32;  // 32x32 MFMA tiles per wave
+  static constexpr int CHUNKS = BK / 8;             // 16-byte chunks per tile row
+  static constexpr int SEG_ROWS = 64 / CHUNKS;      // tile rows per 1 KB wave load
+  static constexpr int SEG_A = BM / SEG_ROWS, SEG_B = BN / SEG_ROWS;
+  static constexpr int LOADS = (SEG_A + SEG_B) / WAVES;  // load instructions per lane per stage
+  static constexpr int STAGE = (BM + BN) * BK;           // bf16 elements per stage
+  static_assert(BK == 32 || BK == 64, "K step");
+  static_assert(LOADS * WAVES == SEG_A + SEG_B && SEG_A % WAVES == 0, "stage load must split evenly over waves");
+  static_assert(MI * 32 == TM && NI * 32 == TN, "wave tile");
+  static_assert(LOADS * (STAGES - 2 > 0 ? STAGES - 2 : 0) <= 63, "vmcnt range");
+  static_assert(STAGES * STAGE * 2 <= 160 * 1024, "LDS");
+  // 16-byte chunk c of tile row r sits at slot c ^ swz(r): any 16 consecutive
+  // rows read at one chunk (one fragment read, 256 bytes per 16 lanes) land
+  // on 16 distinct 16-byte bank groups
+  static __device__ __forceinline__ int swz(int r) { return (r / (16 / CHUNKS)) % CHUNKS; }
+};
+
 // NOUT (1 or 3) is the number of outputs sharing A; it is a template
 // parameter so the Q/K/V projection and the output projection are distinct
 // kernels in profiles.
-template <int BM, int BN, int WM, int NOUT, int EPI>
-__global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
-  constexpr int WN = kWaves / WM;
-  constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
-  constexpr int MI = TM / 32, NI = TN / 32;  // 32x32 MFMA tiles per wave
-  constexpr int SEG_A = BM / 8, SEG_B = BN / 8;  // 1 KB segments per stage
-  constexpr int LOADS = (SEG_A + SEG_B) / kWaves;
-  static_assert(LOADS * kWaves == SEG_A + SEG_B, "stage load must split evenly over waves");
-  __shared__ __attribute__((aligned(16))) bf16 A0[BM * BK], A1[BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 B0[BN * BK], B1[BN * BK];
-  auto abuf = [&](auto s) -> bf16* { if constexpr (decltype(s)::value == 0) return A0; else return A1; };
-  auto bbuf = [&](auto s) -> bf16* { if constexpr (decltype(s)::value == 0) return B0; else return B1; };
+template <class TL, int NOUT, int EPI>
+__global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
+  constexpr int BM = TL::BM, BN = TL::BN, BK = TL::BK, STAGES = TL::STAGES, WN = TL::WN;
+  constexpr int TM = TL::TM, TN = TL::TN, MI = TL::MI, NI = TL::NI, LOADS = TL::LOADS;
+  constexpr int SEG_A = TL::SEG_A, CHUNKS = TL::CHUNKS, SEG_ROWS = TL::SEG_ROWS;
+  // one array per stage, so that the compiler can tell the asynchronous
+  // loads into one stage from the fragment reads of another
+  __shared__ __attribute__((aligned(16))) bf16 L0[TL::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 L1[TL::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 L2[STAGES > 2 ? TL::STAGE : 1];
+  __shared__ __attribute__((aligned(16))) bf16 L3[STAGES > 3 ? TL::STAGE : 1];
+  auto stage = [&](auto s) -> bf16* {
+    if constexpr (decltype(s)::value == 0) return L0;
+    else if constexpr (decltype(s)::value == 1) return L1;
+    else if constexpr (decltype(s)::value == 2) return L2;
+    else return L3;
+  };
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
 
   const int tiles_m = (g.M + BM - 1) / BM;
   const int tiles_n1 = (g.Nc + BN - 1) / BN;  // per output
@@ -87,17 +126,18 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
   const int wm = wave / WN, wn = wave % WN;
   const int l32 = lane & 31, hi = lane >> 5;
 
-  // This lane's rows of the stage loads: segment s = i*8 + wave covers tile
-  // rows 8s .. 8s+7 (A tile first, then B tile); the lane fetches row
-  // 8s + lane/8, global chunk (lane%8) ^ swz(row) into LDS slot lane%8.
+  // This lane's rows of the stage loads: segment s = i*WAVES + wave covers
+  // tile rows SEG_ROWS*s .. (A tile first, then B tile); the lane fetches
+  // row SEG_ROWS*s + lane/CHUNKS, global chunk (lane%CHUNKS) ^ swz(row),
+  // into LDS slot lane%CHUNKS.
   const bf16* src[LOADS];
-  int dst[LOADS];  // element offset of the segment in its tile
+  int dst[LOADS];  // element offset of the segment in its stage
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
-    const int s = i * kWaves + wave;
+    const int s = i * TL::WAVES + wave;
     const bool a = s < SEG_A;
-    const int trow = (a ? s : s - SEG_A) * 8 + lane / 8;
-    const int chunk = (lane % 8) ^ swz(trow);
+    const int trow = (a ? s : s - SEG_A) * SEG_ROWS + lane / CHUNKS;
+    const int chunk = (lane % CHUNKS) ^ TL::swz(trow);
     long grow;
     if (a) {
       const int m = tm * BM + trow;
@@ -109,30 +149,33 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
       grow = (long)n * g.ldb;
     }
     src[i] = (a ? A : B) + grow + chunk * 8;
-    dst[i] = (a ? s : s - SEG_A) * 512;
+    dst[i] = s * 512;  // the B tile follows the A tile in the stage
   }
   auto issue = [&](auto st, int k0) {
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      // segments i*8 + wave: all of one wave's segments of load i lie in the
-      // same tile when SEG_A is a multiple of 8 (always true here)
-      bf16* base = (i * kWaves < SEG_A) ? abuf(st) : bbuf(st);
-      __builtin_amdgcn_global_load_lds((global_cvoid*)(src[i] + k0), (lds_void*)(base + dst[i]), 16, 0, 0);
-    }
+    for (int i = 0; i < LOADS; ++i)
+      __builtin_amdgcn_global_load_lds((global_cvoid*)(src[i] + k0), (lds_void*)(stage(st) + dst[i]), 16, 0, 0);
   };
-  static_assert(SEG_A % kWaves == 0, "A segments must fill whole load rounds");
 
-  // fragment read offsets: row (tile-local) l32 + 32*t, chunk kk*2 + hi
-  const int xr = ((hi ^ swz(l32)) * 8);  // chunk kk*2+hi ^ f = (kk*2) ^ (hi ^ f); f(r) = f(r % 16)
+  // fragment read offsets: row (tile-local) l32 + 32*t, chunk kk*2 + hi;
+  // swz(l32 + 32 t) = swz(l32)
+  const int xr = ((hi ^ TL::swz(l32)) * 8);
   f32x16 acc[MI][NI];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = (f32x16){};
 
-  auto compute = [&](auto st) {
-    const bf16* As = abuf(st) + (wm * TM + l32) * BK;
-    const bf16* Bs = bbuf(st) + (wn * TN + l32) * BK;
+  // compute(st, LG): the MFMAs of one stage. The reads of slice kk+1 are
+  // spread between the MFMAs of slice kk, so their latency hides behind them
+  // (only slice 0 waits for its reads), and the LG stage loads issued just
+  // before (0 or LOADS) are spread one per MFMA over the first slices, so
+  // that they do not hold the wave at their issue ahead of its MFMAs.
+  auto compute = [&](auto st, auto lg) {
+    constexpr int LG = decltype(lg)::value, KS = BK / 16, R = MI + NI, M = MI * NI;
+    static_assert(M >= R, "one MFMA per fragment read at least");
+    const bf16* As = stage(st) + (wm * TM + l32) * BK;
+    const bf16* Bs = stage(st) + BM * BK + (wn * TN + l32) * BK;
     bf16x8 af[2][MI], bfr[2][NI];
     auto ld = [&](int kk, int b) {
       const int off = (kk * 16) ^ xr;
@@ -142,37 +185,75 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
       for (int j = 0; j < NI; ++j) bfr[b][j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * BK + off);
     };
     ld(0, 0);
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      if (kk + 1 < BK / 16) ld(kk + 1, (kk + 1) & 1);
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+    static_for<0, KS>([&](auto kc) {
+      constexpr int kk = decltype(kc)::value;
+      if constexpr (kk + 1 < KS) ld(kk + 1, (kk + 1) & 1);
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i], acc[i][j], 0, 0, 0);
-      if (kk + 1 < BK / 16) {
-        __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, MI * NI, 0);
-      }
-    }
+      static_for<0, M>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (kk + 1 < KS && m < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if constexpr (kk * M + m < LG) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      });
+    });
   };
 
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2 % STAGES>;
+  using S3 = std::integral_constant<int, 3 % STAGES>;
+  using Interleave = std::integral_constant<int, LOADS>;
+  using NoLoads = std::integral_constant<int, 0>;
   const int nk = g.K / BK;
+  // prologue: steps 0 .. STAGES-2 in flight
   issue(S0{}, 0);
-  // step k lives in stage k % 2: wait for its loads, make them visible (and
-  // free the other stage), start step k+1's loads, compute step k
-  auto step = [&](auto st, auto other, int k) {
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  if constexpr (STAGES > 2) if (1 < nk) issue(S1{}, BK);
+  if constexpr (STAGES > 3) if (2 < nk) issue(S2{}, 2 * BK);
+  // step k lives in stage k % STAGES: wait for its loads (the loads of the
+  // up to STAGES-2 later steps may stay in flight; loads complete in order),
+  // make them visible to all waves (which also frees stage (k-1) % STAGES),
+  // start step k+STAGES-1's loads into that stage, compute step k. In the
+  // steady state (full) the loads are unconditional and share the scheduling
+  // region of the MFMAs; near the end of K they are conditional.
+  auto step = [&](auto st, auto nxt, int k, auto full) {
+    if (STAGES > 2 && k + STAGES - 2 < nk) __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS * (STAGES > 2 ? STAGES - 2 : 0)));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
-    if (k + 1 < nk) issue(other, (k + 1) * BK);
-    compute(st);
+    if constexpr (decltype(full)::value) {
+      issue(nxt, (k + STAGES - 1) * BK);
+      compute(st, Interleave{});
+    } else {
+      if (k + STAGES - 1 < nk) issue(nxt, (k + STAGES - 1) * BK);
+      compute(st, NoLoads{});
+    }
   };
-  for (int k = 0; k < nk; k += 2) {
-    step(S0{}, S1{}, k);
-    if (k + 1 < nk) step(S1{}, S0{}, k + 1);
-  }
+  // nxt = (k + STAGES - 1) % STAGES = (k - 1) % STAGES. Whole rounds of
+  // STAGES steps whose loads all fall inside K run in the loop, the remaining
+  // steps after it, so that the loop body has no conditional step (the
+  // accumulators stay in place).
+  auto round = [&](int k, int n, auto full) __attribute__((always_inline)) {
+    if constexpr (STAGES == 2) {
+      step(S0{}, S1{}, k, full);
+      if (n > 1) step(S1{}, S0{}, k + 1, full);
+    } else if constexpr (STAGES == 3) {
+      step(S0{}, S2{}, k, full);
+      if (n > 1) step(S1{}, S0{}, k + 1, full);
+      if (n > 2) step(S2{}, S1{}, k + 2, full);
+    } else {
+      step(S0{}, S3{}, k, full);
+      if (n > 1) step(S1{}, S0{}, k + 1, full);
+      if (n > 2) step(S2{}, S1{}, k + 2, full);
+      if (n > 3) step(S3{}, S2{}, k + 3, full);
+    }
+  };
+  int k = 0;
+  for (; k + 2 * STAGES - 1 <= nk; k += STAGES) round(k, STAGES, std::true_type{});
+  for (; k < nk; k += STAGES) round(k, min(STAGES, nk - k), std::false_type{});
 
   // acc[i][j][e]: output row m = tile row + i*32 + l32,
   //               column n = tile col + j*32 + (e/4)*8 + hi*4 + e%4
@@ -229,33 +310,36 @@ __global__ __launch_bounds__(kThreads) void row_gemm_bf16_kernel(RowGemm g) {
   }
 }
 
-template <int BM, int BN, int WM, int NOUT, int EPI>
+template <class TL, int NOUT, int EPI>
 hipError_t launch(const RowGemm& g, hipStream_t s) {
-  const long tiles = (long)((g.M + BM - 1) / BM) * ((g.Nc + BN - 1) / BN) * NOUT;
-  hipLaunchKernelGGL((row_gemm_bf16_kernel<BM, BN, WM, NOUT, EPI>), dim3((unsigned)tiles),
-                     dim3(kThreads), 0, s, g);
+  const long tiles = (long)((g.M + TL::BM - 1) / TL::BM) * ((g.Nc + TL::BN - 1) / TL::BN) * NOUT;
+  hipLaunchKernelGGL((row_gemm_bf16_kernel<TL, NOUT, EPI>), dim3((unsigned)tiles), dim3(TL::THREADS), 0, s, g);
   return hipGetLastError();
 }
+
+// 256 x 256 tiles (8 waves of 128 x 64) for the three-output projection and
+// for single-output products with at least two workgroups per CU of them;
+// 256 x 128 tiles (8 waves of 64 x 64) for smaller single-output products,
+// whose grid would otherwise leave CUs idle in the last round.
+using TBig = Tiling<256, 256, 64, 2, 8, 2>;
+using TMid = Tiling<256, 128, 64, 2, 8, 4>;
 
 }  // namespace
 
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.Nc <= 0 || (g.n_out != 1 && g.n_out != 3)) return hipSuccess;
-  // 256 x 256 tiles (8 waves of 128 x 64) for the three-output projection and
-  // for single-output products with at least two workgroups per CU of them;
-  // 256 x 128 tiles (8 waves of 64 x 64) for smaller single-output products,
-  // whose grid would otherwise leave CUs idle in the last round.
-  if (g.n_out == 3) return launch<256, 256, 2, 3, kEpiBf16>(g, s);
-  const long big = (long)((g.M + 255) / 256) * ((g.Nc + 255) / 256);
-  if (g.c_f32) return launch<256, 128, 4, 1, kEpiF32>(g, s);
+  if (g.K % TBig::BK || g.K % TMid::BK) return hipErrorInvalidValue;
+  if (g.n_out == 3) return launch<TBig, 3, kEpiBf16>(g, s);
+  const long big = (long)((g.M + TBig::BM - 1) / TBig::BM) * ((g.Nc + TBig::BN - 1) / TBig::BN);
+  if (g.c_f32) return launch<TMid, 1, kEpiF32>(g, s);
   if (big >= 512) {
-    if (g.gelu) return launch<256, 256, 2, 1, kEpiBf16Gelu>(g, s);
-    if (g.residual) return launch<256, 256, 2, 1, kEpiBf16Residual>(g, s);
-    return launch<256, 256, 2, 1, kEpiBf16>(g, s);
+    if (g.gelu) return launch<TBig, 1, kEpiBf16Gelu>(g, s);
+    if (g.residual) return launch<TBig, 1, kEpiBf16Residual>(g, s);
+    return launch<TBig, 1, kEpiBf16>(g, s);
   }
-  if (g.gelu) return launch<256, 128, 4, 1, kEpiBf16Gelu>(g, s);
-  if (g.residual) return launch<256, 128, 4, 1, kEpiBf16Residual>(g, s);
-  return launch<256, 128, 4, 1, kEpiBf16>(g, s);
+  if (g.gelu) return launch<TMid, 1, kEpiBf16Gelu>(g, s);
+  if (g.residual) return launch<TMid, 1, kEpiBf16Residual>(g, s);
+  return launch<TMid, 1, kEpiBf16>(g, s);
 }
 
 }  // namespace hsa
