@@ -178,7 +178,8 @@ def _find(d, suffix):
     return sorted(out)
 
 
-def _short(name, n=90):
+def _short(name, n=100):
+    name = name.replace("hsa::(anonymous namespace)::", "").replace("void ", "", 1)
     return name if len(name) <= n else name[: n - 3] + "..."
 
 

@@ -112,6 +112,35 @@ def test_linear(dtype, n, d_in, d_out, mode):
         assert np.all(np.abs(got - want) <= np.abs(want) * 2.0 ** -7 + 1e-4 * np.abs(want).max())
 
 
+@pytest.mark.parametrize("n,d_in,d_out,mode", [
+    (4059, 192, 8256, "plain"),     # >= 512 tiles of 256 x 256: 3 K steps (odd), ragged rows and columns
+    (4059, 448, 8256, "residual"),  # 7 K steps
+    (2049, 320, 16384, "gelu"),     # 5 K steps, 9 x 64 tiles
+    (700, 64, 768, "plain"),        # 256 x 128 tiles: 1 K step (no steady-state loop)
+    (700, 192, 768, "residual"),    # 3 K steps: one steady-state round then the tail
+    (513, 640, 1000, "gelu"),       # 10 K steps, ragged columns
+])
+def test_linear_k_steps(n, d_in, d_out, mode):
+    """The bf16 product over K step counts that exercise the steady-state
+    loop (loads interleaved with the MFMAs) and its tail, on both tilings."""
+    rng = np.random.default_rng(n * 7 + d_in)
+    x = synth.to_bf16_values(rng.standard_normal((n, d_in)).astype(np.float32))
+    w = synth.to_bf16_values((rng.standard_normal((d_out, d_in)) / np.sqrt(d_in)).astype(np.float32))
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    if mode == "residual":
+        r = synth.to_bf16_values(rng.standard_normal((n, d_out)).astype(np.float32))
+        y = to_dev(r, "bf16")
+        H.hsa_linear(xd, n, wd, y, residual=y)
+        want = oracle.linear(x, w, "bf16", residual=r)
+    else:
+        y = torch.zeros((n, d_out), dtype=torch.bfloat16, device=DEV)
+        H.hsa_linear(xd, n, wd, y, gelu=(mode == "gelu"))
+        prod = x.astype(np.float64) @ w.astype(np.float64).T
+        want = oracle.round_to(oracle.gelu_tanh(prod), "bf16") if mode == "gelu" else oracle.linear(x, w, "bf16")
+    got = host(y)
+    assert np.all(np.abs(got - want) <= np.abs(want) * 2.0 ** -7 + 1e-4 * np.abs(want).max())
+
+
 @pytest.mark.parametrize("N,C,case", [(3000, 64, "normal"), (1000, 16, "normal"), (23, 5, "ties"),
                                       (32760, 64, "normal"), (700, 64, "nan")])
 def test_assign_budgets(N, C, case):
