@@ -145,10 +145,12 @@ def gemm_flops(n_active, d):
     return 2.0 * n_active * d * (3 * d) + 2.0 * n_active * d * d
 
 
-def traffic_from_profile():
+def traffic_from_profile(workload, layout, iteration):
     """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
-    if not os.path.exists(TRAFFIC_FILE):
+    summary, if it was taken on the current kernel source and this is the
+    launch it measured (the Wan-14B block, scattered budgets, iteration 1);
+    else None."""
+    if (workload, layout, iteration) != ("wan14b", "scattered", 1) or not os.path.exists(TRAFFIC_FILE):
         return None
     src_sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
     vals = {}
@@ -617,7 +619,7 @@ def main():
         "peak": PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-        "traffic": traffic_from_profile(),
+        "traffic": traffic_from_profile(args.workload, args.layout, args.iteration),
         "flops_per_launch": attn_fl,
     }
     if args.second_iteration >= 0:

@@ -59,6 +59,7 @@ FULL = [
     ("wan14b", 1, "scattered"),
     ("wan14b", 1, "contiguous"),
     ("wan14b", 2, "scattered"),
+    ("wan14b_720p", 1, "scattered"),  # N = 75600, 18900 active rows
 ]
 
 
