@@ -164,6 +164,17 @@ int hsa_out_scatter(int dtype, const void* o, const int32_t* idx, int32_t n_acti
  * tensor of the dtype. 0 for an unknown dtype or negative sizes. */
 size_t hsa_attention_workspace_bytes(int dtype, int32_t n_active, int32_t d);
 
+/* Workspace bytes with which hsa_active_attention may also split the cached
+ * rows of a bf16 launch into up to 4 key parts: the compact tensor, rounded
+ * up to 256 bytes, then 4 x n_active x heads x (head_dim + 2) fp32 values
+ * (each part's unnormalized output and its softmax maximum and sum). The
+ * library splits only when that fills the compute units better (a grid of
+ * few workgroups: few heads or few active rows) and merges the parts in a
+ * second kernel, an exact rearrangement of the softmax sum. For HSA_STEP_F32
+ * this equals hsa_attention_workspace_bytes. 0 for invalid sizes. */
+size_t hsa_attention_split_workspace_bytes(int dtype, int32_t n_active, int32_t heads,
+                                           int32_t head_dim);
+
 /*
  * Active-query attention followed by the output projection and the scatter
  * of the result (Section 2.3, step 3 and the paragraph after it): for each
@@ -172,7 +183,11 @@ size_t hsa_attention_workspace_bytes(int dtype, int32_t n_active, int32_t d);
  * followed by hsa_out_scatter. Rows of out not in idx are untouched.
  *   workspace       device buffer of at least
  *                   hsa_attention_workspace_bytes(dtype, n_active, d) bytes,
- *                   owned by the caller; its contents are overwritten.
+ *                   owned by the caller; its contents are overwritten. For
+ *                   bf16, the bytes past the compact tensor (from the next
+ *                   256-byte boundary) may hold key parts; with
+ *                   hsa_attention_split_workspace_bytes bytes every split the
+ *                   library chooses fits, with fewer it may split less.
  * out must not overlap q, the caches, wo or the workspace.
  */
 int hsa_active_attention(int dtype, const void* q, const void* k_cache, const void* v_cache,
@@ -402,6 +417,10 @@ typedef struct hsa_stack {
                                      prefix are cached and rewritten at every iteration) */
   void* k_tail;                   /* scratch [N - n_cached, d] dtype shared by the layers */
   void* v_tail;
+  /* optional scratch for key parts of the bf16 attention launches (NULL: no split); with
+     hsa_attention_split_workspace_bytes(dtype, N, heads, head_dim) bytes every split fits */
+  void* attn_parts;
+  int64_t attn_parts_bytes;
 } hsa_stack;
 
 /*

@@ -5,7 +5,12 @@
 // Work split: one workgroup of NW waves per (head, tile of 32*NW active
 // queries); each wave owns 32 queries. Workgroups of one head are placed
 // contiguously on one XCD so concurrently running query tiles stream the same
-// K/V rows through that XCD's L2.
+// K/V rows through that XCD's L2. A launch of few workgroups (few heads or
+// few active rows, e.g. 384 for 12 heads at 25% active on 256 CUs) may also
+// split the cached rows into key parts: each part's workgroup writes its
+// unnormalized output with its softmax maximum and sum (fp32, caller
+// workspace) and attention_combine merges the parts, rescaling each by
+// 2^(m_p - max m) (the softmax of a concatenation).
 //
 // K/V tiles of 64 cached rows go global -> LDS directly (global_load_lds_dwordx4:
 // each wave instruction fills one contiguous 1 KB segment of LDS, lane l at
@@ -56,6 +61,14 @@ constexpr int BKV = 64;                 // cached rows per LDS tile
 constexpr int NBUF = 3;                 // LDS tiles in flight
 constexpr float kSlowSum = 65536.0f;    // 2^16: raise the reference maximum
 
+// Key parts of one launch (split over the cached rows, merged afterwards)
+struct KvParts {
+  int parts;        // 1: no split, the kernel writes o directly
+  int chunk;        // cached rows per part (a multiple of BKV)
+  float* o_part;    // [parts, n_q, d] unnormalized outputs
+  float* ml_part;   // [parts, n_q, heads] (m, l) pairs
+};
+
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void global_cvoid;
@@ -77,7 +90,8 @@ template <int DH, int NW, bool SPLIT>
 __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
     bf16* __restrict__ o, int n_q, int n_kv, int d, float sl2e, int n_qtiles,
-    const bf16* __restrict__ kc2, const bf16* __restrict__ vc2, int n_split) {
+    const bf16* __restrict__ kc2, const bf16* __restrict__ vc2, int n_split, int kv_chunk,
+    int parts, float* __restrict__ o_part, float* __restrict__ ml_part) {
   constexpr int BQ = NW * 32;        // queries per workgroup
   constexpr int CPR = DH / 8;        // 16-byte chunks per cached row
   constexpr int RPS = 64 / CPR;      // rows per 1 KB LDS segment
@@ -99,9 +113,16 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     if constexpr (B == 0) return V0; else if constexpr (B == 1) return V1; else return V2;
   };
 
-  const int item = xcd_contiguous(blockIdx.x, n_qtiles * (d / DH));
-  const int h = item / n_qtiles;
-  const int qt = item - h * n_qtiles;
+  const int heads = d / DH;
+  const int item = xcd_contiguous(blockIdx.x, n_qtiles * heads * parts);
+  const int hp = item / n_qtiles;  // (head, key part); the query tiles of one pair are adjacent
+  const int qt = item - hp * n_qtiles;
+  const int h = hp / parts;
+  const int part = hp - h * parts;
+  // cached rows of this part (all of them when parts == 1); kv_chunk is a
+  // multiple of the tile, so tiles never straddle a part or the segment split
+  const int kv_begin = part * kv_chunk;
+  const int kv_end = min(n_kv, kv_begin + kv_chunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, hi = lane >> 5;
   const long col0 = (long)h * DH;
@@ -188,11 +209,11 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   // they share a scheduling region with the softmax; after the last block
   // they are unused.
   auto step = [&](f32x16& s_cur, f32x16& s_nxt, auto nbuf, int nkb, auto buf, int vb, int key0) {
-    if (key0 + 32 > n_kv) {  // ragged last block: mask the keys beyond N
+    if (key0 + 32 > kv_end) {  // ragged last block: mask the keys beyond the part
       const int kbase = key0 + hi * 4;
 #pragma unroll
       for (int e = 0; e < 16; ++e)
-        if (kbase + (e >> 2) * 8 + (e & 3) >= n_kv) s_cur[e] = -INFINITY;
+        if (kbase + (e >> 2) * 8 + (e & 3) >= kv_end) s_cur[e] = -INFINITY;
     }
     scores(nbuf, nkb, s_nxt);
     float p[16];
@@ -250,9 +271,9 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
   using B2 = std::integral_constant<int, 2>;
-  const int n_tiles = (n_kv + BKV - 1) / BKV;
-  issue_tile(B0{}, 0);
-  if (n_tiles > 1) issue_tile(B1{}, BKV);
+  const int n_tiles = (kv_end - kv_begin + BKV - 1) / BKV;
+  issue_tile(B0{}, kv_begin);
+  if (n_tiles > 1) issue_tile(B1{}, kv_begin + BKV);
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();
   f32x16 sa, sb;
@@ -260,7 +281,7 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   // tile it lives in buffer it % 3; the loop is unrolled by 3 so that every
   // buffer index is a compile-time constant
   auto tile = [&](auto buf, auto nxt, auto nn, int it) {
-    const int kv0 = it * BKV;
+    const int kv0 = kv_begin + it * BKV;
     // block 0 of this tile; the next block is block 1 of the same tile
     step(sa, sb, buf, 32, buf, 0, kv0);
     // tile it+1 (issued one iteration ago) has landed; after this barrier every
@@ -269,7 +290,7 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     __syncthreads();
     if (it + 2 < n_tiles) issue_tile(nn, kv0 + 2 * BKV);
     // block 1 of this tile; the next block is block 0 of tile it+1
-    if (kv0 + 32 < n_kv) step(sb, sa, nxt, 0, buf, 32, kv0 + 32);
+    if (kv0 + 32 < kv_end) step(sb, sa, nxt, 0, buf, 32, kv0 + 32);
   };
   for (int it = 0; it < n_tiles; it += NBUF) {
     tile(B0{}, B1{}, B2{}, it);
@@ -279,9 +300,10 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
 
   // acc[dt][e]: channel dt*32 + (e/4)*8 + hi*4 + e%4 of query l32
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv = 1.f / l_tot;
   const int qrow = qt * BQ + wave * 32 + l32;
-  if (qrow < n_q) {
+  if (qrow >= n_q) return;
+  if (parts == 1) {
+    const float inv = 1.f / l_tot;
     bf16* dst = o + (long)qrow * d + col0;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -292,21 +314,77 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
         *reinterpret_cast<bf16x4*>(dst + dt * 32 + g * 8 + hi * 4) = to_bf16x4(v);
       }
     }
+  } else {
+    // this part's unnormalized output sum_n 2^(s_n - m) v_n, with m (log2
+    // units) and l = sum_n 2^(s_n - m); attention_combine merges the parts
+    const long prow = (long)part * n_q + qrow;
+    float* dst = o_part + prow * d + col0;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(dst + dt * 32 + g * 8 + hi * 4) =
+            (f32x4){acc[dt][4 * g + 0], acc[dt][4 * g + 1], acc[dt][4 * g + 2], acc[dt][4 * g + 3]};
+    }
+    if (hi == 0)
+      *reinterpret_cast<f32x2*>(ml_part + (prow * heads + h) * 2) =
+          (f32x2){have_ref ? m_ref : -INFINITY, l_tot};
+  }
+}
+
+// Merge of the key parts (the softmax of a concatenation): per query row and
+// head, m = max_p m_p, w_p = 2^(m_p - m), o = sum_p w_p O_p / sum_p w_p l_p.
+// One workgroup per query row; each thread produces 4 consecutive channels.
+__global__ __launch_bounds__(256) void attention_combine_kernel(const float* __restrict__ o_part,
+                                                               const float* __restrict__ ml_part,
+                                                               bf16* __restrict__ o, int n_q,
+                                                               int d, int head_dim, int parts) {
+  const int row = blockIdx.x;
+  const int heads = d / head_dim;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const int h = c / head_dim;
+    float mp[kMaxKvParts], lp[kMaxKvParts];
+    float m = -INFINITY;
+#pragma unroll
+    for (int p = 0; p < kMaxKvParts; ++p) {
+      if (p < parts) {
+        const f32x2 ml = *reinterpret_cast<const f32x2*>(ml_part + (((long)p * n_q + row) * heads + h) * 2);
+        mp[p] = ml[0];
+        lp[p] = ml[1];
+        m = fmaxf(m, ml[0]);
+      }
+    }
+    f32x4 acc = {};
+    float l = 0.f;
+#pragma unroll
+    for (int p = 0; p < kMaxKvParts; ++p) {
+      if (p < parts) {
+        const float w = __builtin_amdgcn_exp2f(mp[p] - m);  // 0 for an empty part (m_p = -inf)
+        l += w * lp[p];
+        acc += w * *reinterpret_cast<const f32x4*>(o_part + ((long)p * n_q + row) * d + c);
+      }
+    }
+    *reinterpret_cast<bf16x4*>(o + (long)row * d + c) = to_bf16x4(acc * (1.f / l));
   }
 }
 
 template <int DH, int NW, bool SPLIT>
 hipError_t launch_split(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
                         int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
-                        int n_split) {
+                        int n_split, const KvParts& kp) {
   constexpr int BQ = NW * 32;
   const int n_qtiles = (n_q + BQ - 1) / BQ;
   const int d = heads * DH;
-  hipLaunchKernelGGL((attention_bf16_kernel<DH, NW, SPLIT>), dim3((unsigned)(n_qtiles * heads)),
+  hipLaunchKernelGGL((attention_bf16_kernel<DH, NW, SPLIT>), dim3((unsigned)(n_qtiles * heads * kp.parts)),
                      dim3(NW * 64), 0, s, static_cast<const bf16*>(q),
                      static_cast<const bf16*>(k), static_cast<const bf16*>(v),
                      static_cast<bf16*>(o), n_q, n_kv, d, sl2e, n_qtiles,
-                     static_cast<const bf16*>(k2), static_cast<const bf16*>(v2), n_split);
+                     static_cast<const bf16*>(k2), static_cast<const bf16*>(v2), n_split, kp.chunk,
+                     kp.parts, kp.o_part, kp.ml_part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || kp.parts == 1) return e;
+  hipLaunchKernelGGL(attention_combine_kernel, dim3((unsigned)n_q), dim3(256), 0, s,
+                     kp.o_part, kp.ml_part, static_cast<bf16*>(o), n_q, d, DH, kp.parts);
   return hipGetLastError();
 }
 
@@ -314,19 +392,75 @@ hipError_t launch_split(const void* q, const void* k, const void* v, void* o, in
 template <int DH, int NW>
 hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
                       int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
-                      int n_split) {
+                      int n_split, const KvParts& kp) {
   if (n_split < n_kv) {
     if (n_split % BKV != 0) return hipErrorInvalidValue;
-    return launch_split<DH, NW, true>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
+    return launch_split<DH, NW, true>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
   }
-  return launch_split<DH, NW, false>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
+  return launch_split<DH, NW, false>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
+}
+
+int compute_units() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
+// Key parts for a grid of `wgs` workgroups: the count p <= kMaxKvParts that
+// minimizes the launch's rounds per unit of work, ceil(wgs p / CUs) / p, if
+// that is at least 8% below a single part, each part keeps at least 8 tiles
+// and the workspace holds the partial results; HSA_ATTN_KV_PARTS (1..4)
+// forces a count for measurement sweeps and tests (workspace permitting).
+KvParts choose_kv_parts(int wgs, int n_q, int n_kv, int heads, int head_dim, void* ws,
+                        size_t ws_bytes) {
+  KvParts kp{1, n_kv, nullptr, nullptr};
+  if (!ws || n_kv <= 0) return kp;
+  const int tiles = (n_kv + BKV - 1) / BKV;
+  int p = 1;
+  const char* forced = getenv("HSA_ATTN_KV_PARTS");
+  const int f = forced ? atoi(forced) : 0;
+  if (f >= 1 && f <= kMaxKvParts) {
+    p = f;
+  } else {
+    const int cus = compute_units();
+    const double one = (double)((wgs + cus - 1) / cus);
+    double best = one;
+    for (int c = 2; c <= kMaxKvParts; ++c) {
+      if (tiles < 8 * c) break;
+      const double r = (double)(((long)wgs * c + cus - 1) / cus) / c;
+      if (r < best * 0.999) { best = r; p = c; }
+    }
+    if (best > 0.92 * one) p = 1;
+  }
+  p = std::min(p, tiles);
+  if (p <= 1) return kp;
+  const int chunk = (tiles + p - 1) / p * BKV;  // every part but the last gets `chunk` rows
+  p = (n_kv + chunk - 1) / chunk;               // and none is empty
+  if (p <= 1 || attention_parts_bytes(p, n_q, heads, head_dim) > ws_bytes) return kp;
+  kp.parts = p;
+  kp.chunk = chunk;
+  kp.o_part = static_cast<float*>(ws);
+  kp.ml_part = kp.o_part + (size_t)p * n_q * heads * head_dim;
+  return kp;
 }
 
 }  // namespace
 
+size_t attention_parts_bytes(int parts, int n_q, int heads, int head_dim) {
+  return (size_t)parts * n_q * heads * (head_dim + 2) * sizeof(float);
+}
+
 hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, void* o, int n_q,
                                  int n_kv, int heads, int head_dim, float scale, hipStream_t s,
-                                 const void* k2, const void* v2, int n_split) {
+                                 const void* k2, const void* v2, int n_split, void* ws,
+                                 size_t ws_bytes) {
   if (n_q <= 0) return hipSuccess;
   if (!k2 || !v2) {
     k2 = k;  // any valid pointer: never read
@@ -340,11 +474,13 @@ hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, vo
   const char* forced = getenv("HSA_ATTN_WAVES");
   int nw = forced ? atoi(forced) : 0;
   if (nw != 4 && nw != 8) nw = ((long)((n_q + 255) / 256) * heads >= 256) ? 8 : 4;
+  const int wgs = (n_q + nw * 32 - 1) / (nw * 32) * heads;
+  const KvParts kp = choose_kv_parts(wgs, n_q, n_kv, heads, head_dim, ws, ws_bytes);
   if (head_dim == 64)
-    return nw == 8 ? launch_cfg<64, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split)
-                   : launch_cfg<64, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
-  return nw == 8 ? launch_cfg<128, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split)
-                 : launch_cfg<128, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split);
+    return nw == 8 ? launch_cfg<64, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp)
+                   : launch_cfg<64, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
+  return nw == 8 ? launch_cfg<128, 8>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp)
+                 : launch_cfg<128, 4>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
 }
 
 }  // namespace hsa

@@ -142,10 +142,16 @@ hipError_t launch_row_gemm_f32(const RowGemm& g, hipStream_t s);
 // Keys/values: rows n < n_split come from (k, v), rows n_split .. n_kv-1 from
 // (k2, v2) at row n - n_split (a cache prefix followed by fresh rows). The
 // bf16 kernel needs n_split to be a multiple of 64 (its key tile).
+// bf16 attention. With a workspace of at least attention_parts_bytes(p, ...)
+// bytes the launch may split the cached rows into p <= kMaxKvParts parts
+// (when that fills the CUs better) and merge them in a second kernel.
+constexpr int kMaxKvParts = 4;
+size_t attention_parts_bytes(int parts, int n_q, int heads, int head_dim);
 hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, void* o, int n_q,
                                  int n_kv, int heads, int head_dim, float scale, hipStream_t s,
                                  const void* k2 = nullptr, const void* v2 = nullptr,
-                                 int n_split = 0x7fffffff);
+                                 int n_split = 0x7fffffff, void* ws = nullptr,
+                                 size_t ws_bytes = 0);
 hipError_t launch_attention_f32(const void* q, const void* k, const void* v, void* o, int n_q,
                                 int n_kv, int heads, int head_dim, float scale, hipStream_t s,
                                 const void* k2 = nullptr, const void* v2 = nullptr,

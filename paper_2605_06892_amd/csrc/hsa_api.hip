@@ -102,9 +102,12 @@ HSA_API int hsa_qkv_scatter(int dtype, const void* x, int32_t x_compact, const i
                                               : hsa::launch_row_gemm_f32(g, stream));
 }
 
-HSA_API int hsa_attention_core(int dtype, const void* q, const void* k_cache, const void* v_cache,
-                               int32_t n_active, int64_t n_tokens, int32_t heads,
-                               int32_t head_dim, float scale, void* o, hipStream_t stream) {
+namespace {
+
+// hsa_attention_core with an optional workspace for key parts (bf16 only)
+int attention_core(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                   int32_t n_active, int64_t n_tokens, int32_t heads, int32_t head_dim,
+                   float scale, void* o, void* parts_ws, size_t parts_bytes, hipStream_t stream) {
   const size_t es = elem_size(dtype);
   if (!es) return HSA_STEP_ERR_DTYPE;
   if (heads <= 0 || (head_dim != 64 && head_dim != 128) || n_active < 0 || n_tokens < 0 ||
@@ -121,12 +124,29 @@ HSA_API int hsa_attention_core(int dtype, const void* q, const void* k_cache, co
   const size_t ab = row * (size_t)n_active, cb = row * (size_t)n_tokens;
   if (overlaps(o, ab, q, ab) || overlaps(o, ab, k_cache, cb) || overlaps(o, ab, v_cache, cb))
     return HSA_STEP_ERR_ALIAS;
+  if (parts_ws && (overlaps(parts_ws, parts_bytes, q, ab) || overlaps(parts_ws, parts_bytes, o, ab) ||
+                   overlaps(parts_ws, parts_bytes, k_cache, cb) ||
+                   overlaps(parts_ws, parts_bytes, v_cache, cb)))
+    return HSA_STEP_ERR_ALIAS;
+  if (parts_ws && !aligned(parts_ws, 16)) return HSA_STEP_ERR_SHAPE;
   hipError_t e = dtype == HSA_STEP_BF16
                      ? hsa::launch_attention_bf16(q, k_cache, v_cache, o, n_active, (int)n_tokens,
-                                                  heads, head_dim, scale, stream)
+                                                  heads, head_dim, scale, stream, nullptr, nullptr,
+                                                  0x7fffffff, parts_ws, parts_bytes)
                      : hsa::launch_attention_f32(q, k_cache, v_cache, o, n_active, (int)n_tokens,
                                                  heads, head_dim, scale, stream);
   return launch_status(e);
+}
+
+size_t round_up_256(size_t b) { return (b + 255) / 256 * 256; }
+
+}  // namespace
+
+HSA_API int hsa_attention_core(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                               int32_t n_active, int64_t n_tokens, int32_t heads,
+                               int32_t head_dim, float scale, void* o, hipStream_t stream) {
+  return attention_core(dtype, q, k_cache, v_cache, n_active, n_tokens, heads, head_dim, scale, o,
+                        nullptr, 0, stream);
 }
 
 HSA_API int hsa_out_scatter(int dtype, const void* o, const int32_t* idx, int32_t n_active,
@@ -167,6 +187,14 @@ HSA_API size_t hsa_attention_workspace_bytes(int dtype, int32_t n_active, int32_
   return es * (size_t)n_active * (size_t)d;
 }
 
+HSA_API size_t hsa_attention_split_workspace_bytes(int dtype, int32_t n_active, int32_t heads,
+                                                   int32_t head_dim) {
+  if (heads < 0 || head_dim < 0 || (int64_t)heads * head_dim > INT32_MAX) return 0;
+  const size_t base = hsa_attention_workspace_bytes(dtype, n_active, heads * head_dim);
+  if (dtype != HSA_STEP_BF16 || base == 0) return base;
+  return round_up_256(base) + hsa::attention_parts_bytes(hsa::kMaxKvParts, n_active, heads, head_dim);
+}
+
 HSA_API int hsa_active_attention(int dtype, const void* q, const void* k_cache,
                                  const void* v_cache, const int32_t* idx, int32_t n_active,
                                  int64_t n_tokens, int32_t heads, int32_t head_dim, float scale,
@@ -181,6 +209,13 @@ HSA_API int hsa_active_attention(int dtype, const void* q, const void* k_cache,
   if (n_active == 0) return HSA_STEP_OK;
   const size_t need = hsa_attention_workspace_bytes(dtype, n_active, d);
   if (!workspace || workspace_bytes < need) return HSA_STEP_ERR_WORKSPACE;
+  // bytes past the compact O (from a 256-byte boundary) hold key parts
+  void* parts_ws = nullptr;
+  size_t parts_bytes = 0;
+  if (dtype == HSA_STEP_BF16 && workspace_bytes > round_up_256(need)) {
+    parts_ws = static_cast<char*>(workspace) + round_up_256(need);
+    parts_bytes = workspace_bytes - round_up_256(need);
+  }
   if (!out) return HSA_STEP_ERR_NULL;
   const size_t row = (size_t)d * es;
   const size_t outb = row * (size_t)n_tokens;
@@ -200,8 +235,12 @@ HSA_API int hsa_active_attention(int dtype, const void* q, const void* k_cache,
     return HSA_STEP_ERR_SHAPE;
   if (overlaps(out, outb, wo, row * (size_t)d) || overlaps(out, outb, idx, (size_t)n_active * 4))
     return HSA_STEP_ERR_ALIAS;
-  int st = hsa_attention_core(dtype, q, k_cache, v_cache, n_active, n_tokens, heads, head_dim,
-                              scale, workspace, stream);
+  if (parts_ws && (overlaps(out, outb, parts_ws, parts_bytes) ||
+                   overlaps(wo, row * (size_t)d, parts_ws, parts_bytes) ||
+                   overlaps(idx, (size_t)n_active * 4, parts_ws, parts_bytes)))
+    return HSA_STEP_ERR_ALIAS;
+  int st = attention_core(dtype, q, k_cache, v_cache, n_active, n_tokens, heads, head_dim, scale,
+                          workspace, parts_ws, parts_bytes, stream);
   if (st != HSA_STEP_OK) return st;
   return hsa_out_scatter(dtype, workspace, idx, n_active, n_tokens, d, wo, out, stream);
 }

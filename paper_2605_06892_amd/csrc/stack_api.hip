@@ -340,6 +340,9 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
     written.push_back({s->k_tail, (size_t)n_tail * row_d});
     written.push_back({s->v_tail, (size_t)n_tail * row_d});
   }
+  if (s->attn_parts_bytes < 0 || (s->attn_parts_bytes > 0 && !s->attn_parts)) return HSA_STEP_ERR_SHAPE;
+  const bool parts = s->attn_parts && s->attn_parts_bytes > 0 && s->dtype == HSA_STEP_BF16;
+  if (parts) written.push_back({s->attn_parts, (size_t)s->attn_parts_bytes});
   for (int i = 0; i < 2 * L; ++i) written.push_back({s->caches[i], (size_t)n_rows_cache * row_d});
   std::vector<Span> weights = {{s->w_embed, (size_t)d * row_c}, {s->w_head, (size_t)C * row_d}};
   for (int i = 0; i < 4 * L; ++i) weights.push_back({s->w_layers[i], (size_t)d * row_d});
@@ -391,7 +394,8 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   auto attend = [&](const void* q, const void* k, const void* v, int n_kv, const void* k2 = nullptr,
                     const void* v2 = nullptr, int n_split = 0x7fffffff) {
     return ok(bf ? hsa::launch_attention_bf16(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream,
-                                              k2, v2, n_split)
+                                              k2, v2, n_split, parts ? s->attn_parts : nullptr,
+                                              parts ? (size_t)s->attn_parts_bytes : 0)
                  : hsa::launch_attention_f32(q, k, v, s->o, n, n_kv, s->heads, dh, scale, stream, k2,
                                              v2, n_split));
   };

@@ -57,6 +57,7 @@ def lib() -> ctypes.CDLL:
             "hsa_attention_core": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P]),
             "hsa_out_scatter": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P, P]),
             "hsa_attention_workspace_bytes": (S, [ctypes.c_int, I32, I32]),
+            "hsa_attention_split_workspace_bytes": (S, [ctypes.c_int, I32, I32, I32]),
             "hsa_active_attention": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P, S, P]),
             "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
             "hsa_gather_rows": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P]),
@@ -89,6 +90,7 @@ EXPORTED = (
     "hsa_attention_core",
     "hsa_out_scatter",
     "hsa_attention_workspace_bytes",
+    "hsa_attention_split_workspace_bytes",
     "hsa_active_attention",
     "hsa_cached_euler",
     "hsa_gather_rows",
@@ -130,6 +132,7 @@ class HsaStack(ctypes.Structure):
         ("reserved2", ctypes.c_int32),
         ("prefix_cache", ctypes.c_int32), ("reserved3", ctypes.c_int32), ("n_cached", ctypes.c_int64),
         ("k_tail", ctypes.c_void_p), ("v_tail", ctypes.c_void_p),
+        ("attn_parts", ctypes.c_void_p), ("attn_parts_bytes", ctypes.c_int64),
     ]
 
 
@@ -217,6 +220,11 @@ def hsa_out_scatter(o, idx, n_active: int, wo, out, stream=None) -> None:
 
 def hsa_attention_workspace_bytes(dtype: torch.dtype, n_active: int, d: int) -> int:
     return int(lib().hsa_attention_workspace_bytes(_dtype(torch.empty(0, dtype=dtype)), n_active, d))
+
+
+def hsa_attention_split_workspace_bytes(dtype: torch.dtype, n_active: int, heads: int, head_dim: int) -> int:
+    return int(lib().hsa_attention_split_workspace_bytes(_dtype(torch.empty(0, dtype=dtype)), n_active, heads,
+                                                          head_dim))
 
 
 def hsa_active_attention(q, k_cache, v_cache, idx, n_active: int, heads: int, head_dim: int,
@@ -351,14 +359,15 @@ def hsa_rope_table(theta: float, head_dim: int, grid) -> torch.Tensor:
 def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_active, xa, h, q, o, v_fresh,
                keys, row_scale, heads: int, head_dim: int, cross=None, ffn=None, f=None,
                v_prev=None, rope_cs=None, pos=None, grid=(0, 0, 0), n_cached=None, k_tail=None,
-               v_tail=None) -> HsaStack:
+               v_tail=None, attn_parts=None) -> HsaStack:
     """Fill a struct hsa_stack from device tensors. layers: per layer
     (wq, wk, wv, wo); caches: per layer (k_hat, v_hat); cross: per layer
-    (wq_c, wo_c, k_c, v_c) or None; ffn: per layer (w1, w2) or None. The
+    (wq_c, wo_c, k_c, v_c) or None; ffn: per layer (w1, w2) or None;
+    attn_parts: scratch for key parts of the attention launches or None. The
     returned struct keeps its host pointer arrays alive; the tensors must
     outlive it."""
     ts = [x, v_hat, budget, w_embed, w_head, idx, n_active, xa, h, q, o, v_fresh, keys, row_scale, f, v_prev,
-          rope_cs, pos, k_tail, v_tail]
+          rope_cs, pos, k_tail, v_tail, attn_parts]
     ts += [t for lw in layers for t in lw] + [t for c in caches for t in c]
     ts += [t for lw in (cross or ()) for t in lw] + [t for lw in (ffn or ()) for t in lw]
     _dev(*ts)
@@ -381,7 +390,9 @@ def make_stack(*, x, v_hat, budget, w_embed, w_head, layers, caches, idx, n_acti
                  grid_f=grid[0], grid_h=grid[1], grid_w=grid[2], reserved2=0,
                  prefix_cache=0 if n_cached is None else 1, reserved3=0,
                  n_cached=0 if n_cached is None else int(n_cached),
-                 k_tail=0 if k_tail is None else k_tail.data_ptr(), v_tail=0 if v_tail is None else v_tail.data_ptr())
+                 k_tail=0 if k_tail is None else k_tail.data_ptr(), v_tail=0 if v_tail is None else v_tail.data_ptr(),
+                 attn_parts=0 if attn_parts is None else attn_parts.data_ptr(),
+                 attn_parts_bytes=0 if attn_parts is None else attn_parts.numel() * attn_parts.element_size())
     keep = [wl, cl]
     if cross:
         xl = (ctypes.c_void_p * (4 * len(cross)))(*[t.data_ptr() for lw in cross for t in lw])

@@ -48,6 +48,7 @@ class StackBuffers:
     n_cached: int | None = None          # prefix-only cache: rows per layer cache
     k_tail: torch.Tensor | None = None   # [N - n_cached, d] fresh baseline keys
     v_tail: torch.Tensor | None = None
+    attn_parts: torch.Tensor | None = None  # uint8 scratch: key parts of the attention launches
     _handle: H.HsaStack | None = field(default=None, repr=False)
 
     @property
@@ -64,16 +65,23 @@ class StackBuffers:
 
     @classmethod
     def allocate(cls, N: int, C: int, n_layers: int, heads: int, head_dim: int, dtype: torch.dtype,
-                 device="cuda", ffn: int = 0, ctx: int = 0, n_cached: int | None = None) -> "StackBuffers":
+                 device="cuda", ffn: int = 0, ctx: int = 0, n_cached: int | None = None,
+                 kv_parts: bool = True) -> "StackBuffers":
         """Tensors for N tokens, C latent values per token, n_layers layers of
         width heads * head_dim; ffn > 0 / ctx > 0 add the FFN and
         cross-attention sub-layers of full blocks; n_cached (prefix-only
         cache of reordered tokens, Section 2.5) sizes each layer's cache to
-        the non-baseline prefix."""
+        the non-baseline prefix; kv_parts adds the scratch with which bf16
+        attention launches of few workgroups split their cached rows."""
         d = heads * head_dim
         e = lambda *s, dt=dtype: torch.empty(*s, dtype=dt, device=device)  # noqa: E731
         f32 = torch.float32
         rows = N if n_cached is None else n_cached
+        parts = None
+        if kv_parts and dtype == torch.bfloat16:
+            nb = H.hsa_attention_split_workspace_bytes(dtype, N, heads, head_dim) - \
+                H.hsa_attention_workspace_bytes(dtype, N, d)
+            parts = torch.empty(max(nb, 1), dtype=torch.uint8, device=device)
         tail = None if n_cached is None else N - n_cached
         return cls(x=e(N, C, dt=f32), v_hat=e(N, C, dt=f32), budget=e(N, dt=torch.int32),
                    w_embed=e(d, C), w_head=e(C, d),
@@ -86,7 +94,7 @@ class StackBuffers:
                    v_prev=e(N, C, dt=f32), heads=heads, head_dim=head_dim,
                    cross=[(e(d, d), e(d, d), e(ctx, d), e(ctx, d)) for _ in range(n_layers)] if ctx else None,
                    ffn=[(e(ffn, d), e(d, ffn)) for _ in range(n_layers)] if ffn else None,
-                   f=e(N, ffn) if ffn else None)
+                   f=e(N, ffn) if ffn else None, attn_parts=parts)
 
     def enable_rope(self, grid, theta: float = 10000.0, pos: torch.Tensor | None = None) -> None:
         """Rotate Q and K by the tokens' positions in the latent grid (F, H, W)
@@ -114,7 +122,7 @@ class StackBuffers:
                                         heads=self.heads, head_dim=self.head_dim, cross=self.cross,
                                         ffn=self.ffn, f=self.f, v_prev=self.v_prev, rope_cs=self.rope_cs,
                                         pos=self.pos, grid=self.grid, n_cached=self.n_cached,
-                                        k_tail=self.k_tail, v_tail=self.v_tail)
+                                        k_tail=self.k_tail, v_tail=self.v_tail, attn_parts=self.attn_parts)
         return self._handle
 
 

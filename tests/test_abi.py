@@ -73,6 +73,14 @@ def test_workspace_bytes(lib):
     assert lib.hsa_attention_workspace_bytes(F32, 10, 256) == 10 * 256 * 4
     assert lib.hsa_attention_workspace_bytes(7, 10, 256) == 0
     assert lib.hsa_attention_workspace_bytes(BF16, -1, 256) == 0
+    # the compact tensor from a 256-byte boundary, then 4 parts of fp32 (O, m, l)
+    base = 8190 * 1536 * 2
+    assert lib.hsa_attention_split_workspace_bytes(BF16, 8190, 12, 128) == \
+        (base + 255) // 256 * 256 + 4 * 8190 * 12 * (128 + 2) * 4
+    assert lib.hsa_attention_split_workspace_bytes(BF16, 10, 1, 64) == 1280 + 4 * 10 * 66 * 4
+    assert lib.hsa_attention_split_workspace_bytes(F32, 10, 4, 64) == 10 * 256 * 4
+    assert lib.hsa_attention_split_workspace_bytes(BF16, -1, 4, 64) == 0
+    assert lib.hsa_attention_split_workspace_bytes(BF16, 10, -4, 64) == 0
 
 
 def test_build_active_set_errors(lib):
@@ -130,6 +138,9 @@ def test_attention_errors(lib):
     assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, None, need, None) == WORKSPACE
     assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, W, need - 1, None) == WORKSPACE
     assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, G, need, None) == ALIAS
+    # out inside the key-part bytes past the compact tensor
+    assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, W + 8192, W, 1 << 20, None) == ALIAS
+    assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, W + 8192, G, W, 1 << 20, None) == ALIAS  # wo
     assert g(BF16, A, B, C, None, 10, 100, 4, 64, 0.125, E, G, W, need, None) == NULL
     assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, None, W, need, None) == NULL
     h = lib.hsa_out_scatter
@@ -293,6 +304,9 @@ def test_stack_iteration_errors(lib):
     assert call(s) == ALIAS                                            # a weight inside a cache
     assert call(_stack(q=0x7E0000000000 + 8 * (1 << 32) + 32)[0]) == ALIAS  # q inside h
     assert call(_stack(o=0x7E0000000000 + 3)[0]) == SHAPE              # misaligned
+    assert call(_stack(attn_parts_bytes=-1)[0]) == SHAPE
+    assert call(_stack(attn_parts_bytes=4096)[0]) == SHAPE             # bytes without a buffer
+    assert call(_stack(attn_parts=0x7E0000000000 + 2 * (1 << 32) + 64, attn_parts_bytes=4096)[0]) == ALIAS  # inside x
 
 
 def test_l1_rel_and_key_assignment_errors(lib):

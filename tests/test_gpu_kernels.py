@@ -302,6 +302,88 @@ def test_active_attention_equals_core_then_projection():
     assert torch.equal(ws.view(nA, d), o)
 
 
+def _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, scale, ws_bytes):
+    """hsa_active_attention with a workspace of ws_bytes; returns (compact
+    attention output, out)."""
+    nA, d = q_np.shape
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=DEV)
+    out = to_dev(out0, "bf16")
+    H.hsa_active_attention(to_dev(q_np, "bf16"), to_dev(k_np, "bf16"), to_dev(v_np, "bf16"), i32(idx_np), nA,
+                           heads, dh, scale, to_dev(wo_np, "bf16"), out, ws)
+    o = ws[: nA * d * 2].view(torch.bfloat16).view(nA, d)
+    return host(o), out
+
+
+@pytest.mark.parametrize("parts", [2, 3, 4])
+@pytest.mark.parametrize("N,nA,heads,dh", [(1111, 777, 3, 128), (4100, 300, 2, 64), (130, 70, 2, 128),
+                                           (65, 33, 1, 128), (2048, 256, 4, 128)])
+def test_attention_key_parts(parts, N, nA, heads, dh, monkeypatch):
+    """Cached rows split into key parts (forced count, clamped to the tiles)
+    and merged: the attention output matches the oracle, the projection of
+    it lands on the active rows only."""
+    monkeypatch.setenv("HSA_ATTN_KV_PARTS", str(parts))
+    d = heads * dh
+    rng = np.random.default_rng(N * 10 + parts)
+    q_np, k_np, v_np = (synth.to_bf16_values(rng.standard_normal((r, d)).astype(np.float32)) for r in (nA, N, N))
+    wo_np = synth.to_bf16_values((rng.standard_normal((d, d)) / math.sqrt(d)).astype(np.float32))
+    out0 = synth.to_bf16_values(rng.standard_normal((N, d)).astype(np.float32))
+    idx_np = np.sort(rng.choice(N, nA, replace=False))
+    scale = 1.0 / math.sqrt(dh)
+    ws_bytes = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh)
+    o, out = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, scale, ws_bytes)
+    ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, scale), "bf16")
+    assert rel_inf(o, ref) <= TOL["bf16"]
+    skipped = np.setdiff1d(np.arange(N), idx_np)
+    np.testing.assert_array_equal(host_bits(out)[skipped], host_bits(to_dev(out0, "bf16"))[skipped])
+    assert rel_inf(host(out)[idx_np], oracle.project(o, wo_np, "bf16")) <= 1e-2
+
+
+def test_attention_key_parts_shift_safe(monkeypatch):
+    """Parts whose maxima differ by hundreds (log2 units) merge without
+    overflow or underflow of the kept terms."""
+    monkeypatch.setenv("HSA_ATTN_KV_PARTS", "4")
+    N, nA, heads, dh = 2048, 130, 1, 128
+    rng = np.random.default_rng(5)
+    q_np = synth.to_bf16_values(rng.standard_normal((nA, dh)).astype(np.float32) * 8)
+    k_np = rng.standard_normal((N, dh)).astype(np.float32) * 8
+    k_np[: N // 2] *= 0.05  # the first parts see far smaller scores than the last
+    k_np = synth.to_bf16_values(k_np)
+    v_np = synth.to_bf16_values(rng.standard_normal((N, dh)).astype(np.float32))
+    wo_np = synth.to_bf16_values(np.eye(dh, dtype=np.float32))
+    idx_np = np.arange(nA)
+    out0 = np.zeros((N, dh), np.float32)
+    ws_bytes = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh)
+    o, _ = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, 1.0, ws_bytes)
+    ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, 1.0), "bf16")
+    assert np.all(np.isfinite(o))
+    assert rel_inf(o, ref) <= TOL["bf16"]
+
+
+def test_attention_key_parts_auto_and_minimum_workspace():
+    """A launch of few workgroups (one head, 256 queries, 4096 keys) splits
+    on its own with the split workspace and matches the oracle; with the
+    minimum workspace it does not split and equals hsa_attention_core bit for
+    bit."""
+    N, nA, heads, dh = 4096, 256, 1, 128
+    rng = np.random.default_rng(11)
+    q_np, k_np, v_np = (synth.to_bf16_values(rng.standard_normal((r, dh)).astype(np.float32)) for r in (nA, N, N))
+    wo_np = synth.to_bf16_values((rng.standard_normal((dh, dh)) / math.sqrt(dh)).astype(np.float32))
+    out0 = np.zeros((N, dh), np.float32)
+    idx_np = np.arange(nA)
+    scale = 1.0 / math.sqrt(dh)
+    ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, scale), "bf16")
+    split = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh)
+    o_split, _ = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, scale, split)
+    assert rel_inf(o_split, ref) <= TOL["bf16"]
+    minimum = H.hsa_attention_workspace_bytes(torch.bfloat16, nA, heads * dh)
+    o_min, _ = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, scale, minimum)
+    o_core = torch.empty(nA, dh, dtype=torch.bfloat16, device=DEV)
+    H.hsa_attention_core(to_dev(q_np, "bf16"), to_dev(k_np, "bf16"), to_dev(v_np, "bf16"), nA, heads, dh, scale,
+                         o_core)
+    np.testing.assert_array_equal(o_min, host(o_core))
+    assert not np.array_equal(o_split, o_min)  # the split path ran (different rounding order)
+
+
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("dh", [64, 128])
 def test_attention_every_tile_config(waves, dh, monkeypatch):
