@@ -400,19 +400,6 @@ hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int 
   return launch_split<DH, NW, false>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
 }
 
-int compute_units() {
-  static int cus = 0;
-  if (!cus) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-      cus = n;
-    else
-      cus = 256;
-  }
-  return cus;
-}
-
 // Key parts for a grid of `wgs` workgroups: the count p <= kMaxKvParts that
 // minimizes the launch's rounds per unit of work, ceil(wgs p / CUs) / p, if
 // that is at least 8% below a single part, each part keeps at least 8 tiles

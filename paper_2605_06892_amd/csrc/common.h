@@ -28,6 +28,19 @@ __device__ __forceinline__ int xcd_contiguous(int L, int total) {
   return xcd * base + (xcd < rem ? xcd : rem) + slot;
 }
 
+// Compute units of the current device (queried once; 256 if the query fails).
+inline int compute_units() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0, n = 0;
+    cus = (hipGetDevice(&dev) == hipSuccess &&
+           hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+              ? n
+              : 256;
+  }
+  return cus;
+}
+
 // Round fp32 to bf16, nearest-even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ bf16x4 to_bf16x4(f32x4 v) { return __builtin_convertvector(v, bf16x4); }
 
