@@ -317,31 +317,44 @@ hipError_t launch(const RowGemm& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// 256 x 256 tiles (8 waves of 128 x 64), the faster tiling per FLOP, for every
-// product but the narrow fp32 velocity head and grids where even 256 x 128
-// tiles (8 waves of 64 x 64) fit in one round while 256 x 256 tiles would
-// leave at least half of the CUs idle. Measured on the stack shapes (d = 1536,
-// 8190-32760 rows): 256 x 256 is as fast or faster in every case, by up to
-// 26% where the 256 x 128 grid takes two rounds.
+// Three tilings of 8 waves. Per FLOP 256 x 256 (waves of 128 x 64) is the
+// fastest; 256 x 192 (waves of 64 x 96) costs about 1.14x and 256 x 128
+// (waves of 64 x 64) about 1.35x (measured on the stack shapes), but their
+// finer grids can fill the last round of a launch better. Each launch takes
+// the tiling with the least estimated time, rounds x cost per round, with
+// rounds = ceil(tiles / CUs) and the per-round cost relative to 256 x 256
+// (tile area x cost per FLOP): 1, 0.855, 0.675. A tiling other than 256 x 256
+// must win by 3%. The narrow fp32 velocity head always takes 256 x 128.
 using TBig = Tiling<256, 256, 64, 2, 8, 2>;
+using T192 = Tiling<256, 192, 64, 2, 8, 4>;
 using TMid = Tiling<256, 128, 64, 2, 8, 4>;
+
+template <class TL>
+double estimate(const RowGemm& g, double per_round) {
+  const long tiles = (long)((g.M + TL::BM - 1) / TL::BM) * ((g.Nc + TL::BN - 1) / TL::BN) * g.n_out;
+  const long cus = compute_units();
+  return (double)((tiles + cus - 1) / cus) * per_round;
+}
+
+template <int NOUT, int EPI>
+hipError_t launch_best(const RowGemm& g, hipStream_t s) {
+  const double eb = estimate<TBig>(g, 1.0), e192 = estimate<T192>(g, 0.855),
+               em = estimate<TMid>(g, 0.675);
+  if (e192 < 0.97 * eb && e192 <= em) return launch<T192, NOUT, EPI>(g, s);
+  if (em < 0.97 * eb && em < e192) return launch<TMid, NOUT, EPI>(g, s);
+  return launch<TBig, NOUT, EPI>(g, s);
+}
 
 }  // namespace
 
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.Nc <= 0 || (g.n_out != 1 && g.n_out != 3)) return hipSuccess;
-  if (g.K % TBig::BK || g.K % TMid::BK) return hipErrorInvalidValue;
-  if (g.n_out == 3) return launch<TBig, 3, kEpiBf16>(g, s);
+  if (g.K % TBig::BK || g.K % T192::BK || g.K % TMid::BK) return hipErrorInvalidValue;
+  if (g.n_out == 3) return launch_best<3, kEpiBf16>(g, s);
   if (g.c_f32) return launch<TMid, 1, kEpiF32>(g, s);
-  const long big = (long)((g.M + TBig::BM - 1) / TBig::BM) * ((g.Nc + TBig::BN - 1) / TBig::BN);
-  if (2 * big > compute_units()) {
-    if (g.gelu) return launch<TBig, 1, kEpiBf16Gelu>(g, s);
-    if (g.residual) return launch<TBig, 1, kEpiBf16Residual>(g, s);
-    return launch<TBig, 1, kEpiBf16>(g, s);
-  }
-  if (g.gelu) return launch<TMid, 1, kEpiBf16Gelu>(g, s);
-  if (g.residual) return launch<TMid, 1, kEpiBf16Residual>(g, s);
-  return launch<TMid, 1, kEpiBf16>(g, s);
+  if (g.gelu) return launch_best<1, kEpiBf16Gelu>(g, s);
+  if (g.residual) return launch_best<1, kEpiBf16Residual>(g, s);
+  return launch_best<1, kEpiBf16>(g, s);
 }
 
 }  // namespace hsa

@@ -154,6 +154,7 @@ def _block(N, d, dtype, seed):
     ("bf16", 1000, 256, 0.3, False),
     ("bf16", 1000, 256, 0.3, True),
     ("bf16", 3000, 320, 0.5, False),   # 320 = 2.5 column tiles of 128
+    ("bf16", 10000, 1536, 0.8, False),  # ~8000 rows x 3 x 1536: the 256 x 192 tiling
     ("bf16", 200, 64, 1.0, False),
     ("f32", 1024, 256, 0.33, False),
     ("f32", 333, 100, 0.5, True),

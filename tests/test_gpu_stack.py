@@ -113,9 +113,9 @@ def test_linear(dtype, n, d_in, d_out, mode):
 
 
 @pytest.mark.parametrize("n,d_in,d_out,mode", [
-    (4059, 192, 8256, "plain"),     # 528 tiles of 256 x 256: 3 K steps (odd), ragged rows and columns
+    (4059, 192, 8256, "plain"),     # 256 x 192 tiles (16 x 43): 3 K steps (odd), ragged rows and columns
     (4059, 448, 8256, "residual"),  # 7 K steps
-    (2049, 320, 16384, "gelu"),     # 5 K steps, 9 x 64 tiles
+    (2049, 320, 16384, "gelu"),     # 256 x 256 tiles (9 x 64): 5 K steps
     (700, 64, 768, "plain"),        # 256 x 128 tiles (a grid of few tiles): 1 K step (no steady-state loop)
     (700, 192, 768, "residual"),    # 3 K steps: one steady-state round then the tail
     (513, 640, 1000, "gelu"),       # 10 K steps, ragged columns
