@@ -455,12 +455,13 @@ hipError_t launch_attention_bf16(const void* q, const void* k, const void* v, vo
     n_split = n_kv;
   }
   const float sl2e = scale * 1.4426950408889634f;
-  // Workgroup shape: 8 waves (two per SIMD, 256 queries) whenever that still
-  // gives every CU a workgroup, else 4 waves (128 queries). HSA_ATTN_WAVES
-  // (4 or 8) forces a shape for measurement sweeps.
+  // Workgroup shape: 8 waves (two per SIMD, 256 queries). Measured, 4 waves
+  // (one per SIMD, 128 queries) is slower even where 8-wave workgroups leave
+  // CUs idle (12 heads at 16% active: 640 against 1130 TFLOP/s); key parts
+  // fill such grids instead. HSA_ATTN_WAVES=4 forces the 4-wave shape for
+  // measurement sweeps and tests.
   const char* forced = getenv("HSA_ATTN_WAVES");
-  int nw = forced ? atoi(forced) : 0;
-  if (nw != 4 && nw != 8) nw = ((long)((n_q + 255) / 256) * heads >= 256) ? 8 : 4;
+  const int nw = (forced && atoi(forced) == 4) ? 4 : 8;
   const int wgs = (n_q + nw * 32 - 1) / (nw * 32) * heads;
   const KvParts kp = choose_kv_parts(wgs, n_q, n_kv, heads, head_dim, ws, ws_bytes);
   if (head_dim == 64)
