@@ -500,11 +500,17 @@ def test_tiny_prefix_cache_trajectory():
     assert rel_inf(host(S.restore_order(b, perm)), base[-1]["x"]) <= TOL["f32"]
 
 
-def test_prefix_cache_equals_full_cache_bitwise():
+@pytest.mark.parametrize("kv_parts", [None, "4"])
+def test_prefix_cache_equals_full_cache_bitwise(kv_parts, monkeypatch):
     """At the Wan-1.3B shape (3 layers, RoPE, HSA-75A groups with a 25%
     baseline group reordered to the end) the prefix-only cache changes only
     where the baseline rows' keys live: latents, velocities and the cached
-    prefix rows are bit-identical to the full-cache run."""
+    prefix rows are bit-identical to the full-cache run. The 25%-active
+    iteration splits its attention keys (2 parts by the launcher's choice,
+    or 4 forced), so parts that span the cache prefix and the fresh tail
+    are covered too."""
+    if kv_parts:
+        monkeypatch.setenv("HSA_ATTN_KV_PARTS", kv_parts)
     wl = synth.WORKLOADS["wan1.3b_stack"]
     N, L = wl.N, 3
     wts = synth.draw_stack(wl, seed=7, layers=L)
