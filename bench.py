@@ -59,6 +59,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-schedules", action="store_true", help="skip the preset-schedule trajectories")
     p.add_argument("--no-euler-stress", action="store_true", help="skip the Euler bandwidth-stress shape")
+    p.add_argument("--no-extra-timings", action="store_true",
+                   help="skip the 100%%-active, cold-cache and other-layout timings of the step")
     p.add_argument("--no-end-to-end", action="store_true",
                    help="skip the 30-layer sampling loops (HSA vs dense, T = 40)")
     p.add_argument("--end-to-end-only", action="store_true", help="run only the 30-layer sampling loops")
@@ -118,7 +120,14 @@ def run_step(b, eul, T, it, sigmas, ev=None, margin=0, outside_period=1):
     return n
 
 
-def time_iteration(b, eul, wl, it, sigmas, steps, warmup):
+KERNEL_NAMES = ["active_set", "qkv_scatter", "attention", "out_scatter", "cached_euler"]
+
+
+def time_iteration(b, eul, wl, it, sigmas, steps, warmup, flush=None):
+    """Mean per-call event times over `steps` passes of iteration `it`, the
+    host wall time per pass and the layer-step time (Q/K/V + attention +
+    output) of every pass. With `flush` (a device buffer of at least the
+    MALL's size) it is overwritten before every pass (cold caches)."""
     import torch
 
     for _ in range(warmup):
@@ -128,13 +137,21 @@ def time_iteration(b, eul, wl, it, sigmas, steps, warmup):
     t0 = time.perf_counter()
     n = 0
     for s in range(steps):
+        if flush is not None:
+            flush.zero_()
         n = run_step(b, eul, wl.T, it, sigmas, evs[s])
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps * 1e3
-    names = ["active_set", "qkv_scatter", "attention", "out_scatter", "cached_euler"]
     per = {nm: float(np.mean([evs[s][k].elapsed_time(evs[s][k + 1]) for s in range(steps)]))
-           for k, nm in enumerate(names)}
-    return n, wall, per
+           for k, nm in enumerate(KERNEL_NAMES)}
+    layer = [evs[s][1].elapsed_time(evs[s][4]) for s in range(steps)]
+    return n, wall, per, layer
+
+
+def dist(xs):
+    """Median, 10th and 90th percentile (ms)."""
+    return {"median": round(float(np.median(xs)), 4), "p10": round(float(np.percentile(xs, 10)), 4),
+            "p90": round(float(np.percentile(xs, 90)), 4)}
 
 
 def attention_flops(n_active, N, d):
@@ -579,7 +596,7 @@ def main():
                           "copy_bytes": None if big is None else big.numel() * 4}))
         return
 
-    n, wall, per = time_iteration(b, eul, wl, args.iteration, sigmas, args.steps, args.warmup)
+    n, wall, per, layer = time_iteration(b, eul, wl, args.iteration, sigmas, args.steps, args.warmup)
     layer_ms = per["qkv_scatter"] + per["attention"] + per["out_scatter"]
     attn_fl = attention_flops(n, wl.N, wl.d)
     attn_tflops = attn_fl / (per["attention"] * 1e-3) / 1e12
@@ -608,6 +625,7 @@ def main():
             "euler_state": f"{wl.N}x{EULER_CHANNELS} fp32",
         },
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "layer_step_ms_dist": dist(layer),
         "active_attention_tflops": round(attn_tflops, 2),
         "qkv_out_gemm_tflops": round(gemm_tf, 2),
         "euler_gbs": round(euler_bytes / (per["cached_euler"] * 1e-3) / 1e9, 1),
@@ -622,17 +640,35 @@ def main():
         "traffic": traffic_from_profile(args.workload, args.layout, args.iteration),
         "flops_per_launch": attn_fl,
     }
-    if args.second_iteration >= 0:
-        n2, wall2, per2 = time_iteration(b, eul, wl, args.second_iteration, sigmas, args.steps, 1)
-        out["second"] = {
-            "iteration": args.second_iteration,
+    def item(it, steps, flush=None):
+        n2, wall2, per2, layer2 = time_iteration(b, eul, wl, it, sigmas, steps, 1, flush)
+        return {
+            "iteration": it,
             "n_active": n2,
             "active_fraction": round(n2 / wl.N, 4),
             "layer_step_ms": round(per2["qkv_scatter"] + per2["attention"] + per2["out_scatter"], 4),
+            "layer_step_ms_dist": dist(layer2),
             "ms_per_step": round(wall2, 4),
             "kernels_ms": {k: round(v, 4) for k, v in per2.items()},
             "active_attention_tflops": round(attention_flops(n2, wl.N, wl.d) / (per2["attention"] * 1e-3) / 1e12, 2),
         }
+
+    if args.second_iteration >= 0:
+        out["second"] = item(args.second_iteration, args.steps)
+    if not args.no_extra_timings:
+        # the same step with every token active (iteration T/s_min: the dense comparator, same kernels)
+        full_it = wl.T // min(g[0] for g in wl.groups)
+        out["full_active"] = item(full_it, max(3, args.steps // 4))
+        out["full_active"]["hsa_step_over_full"] = round(layer_ms / out["full_active"]["layer_step_ms"], 4)
+        # cold caches: a 1 GiB buffer (4x the 256 MB MALL) overwritten before every pass
+        flush = torch.empty(256 << 20, dtype=torch.float32, device=dev)
+        out["cold"] = item(args.iteration, max(5, args.steps // 2), flush)
+        del flush
+        # the other budget layout: groups as consecutive index ranges
+        other = "contiguous" if args.layout == "scattered" else "scattered"
+        b.budget.copy_(torch.from_numpy(synth.assign_budgets(blk["v_group"], wl.groups, other)))
+        out["layout_" + other] = item(args.iteration, args.steps)
+        b.budget.copy_(torch.from_numpy(budget))
     if not args.no_euler_stress:
         out["euler_stress"] = euler_stress(dev)
     if not args.no_schedules or not args.no_end_to_end:
