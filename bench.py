@@ -521,18 +521,19 @@ def cpu_baseline(wl, blk, budget, it):
     w = {k: blk[k] for k in ("wq", "wk", "wv", "wo")}
     rng = np.random.default_rng(0)
     times = {}
-    for s in (256, 512):
+    lo, hi = 512, 2048  # about 10 s of oracle work on 16 host threads
+    for s in (lo, hi):
         sub = np.sort(rng.choice(idx, size=min(s, idx.size), replace=False))
         t0 = time.perf_counter()
         oracle.layer_step(blk["x"], sub, w, k0, v0, out0, wl.heads, wl.dh, 1 / math.sqrt(wl.dh), "bf16")
         times[s] = time.perf_counter() - t0
-    per_row = max((times[512] - times[256]) / 256.0, 0.0)
-    fixed = max(times[256] - 256 * per_row, 0.0)
+    per_row = max((times[hi] - times[lo]) / (hi - lo), 0.0)
+    fixed = max(times[lo] - lo * per_row, 0.0)
     est_ms = (fixed + per_row * idx.size) * 1e3
     return {"value": round(est_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
             "host_cpus": os.cpu_count(),
-            "sample": (f"oracle.layer_step on 256 and 512 of the {idx.size} active rows (all {wl.N} cached rows, "
-                       f"{wl.heads} heads), {times[256]:.1f}s + {times[512]:.1f}s; linear fit extrapolated to "
+            "sample": (f"oracle.layer_step on {lo} and {hi} of the {idx.size} active rows (all {wl.N} cached rows, "
+                       f"{wl.heads} heads), {times[lo]:.1f}s + {times[hi]:.1f}s; linear fit extrapolated to "
                        f"all {idx.size} active rows")}
 
 
