@@ -151,6 +151,22 @@ int hsa_attention_core(int dtype, const void* q, const void* k_cache, const void
                        float scale, void* o, hipStream_t stream);
 
 /*
+ * hsa_attention_core with a caller scratch for key parts (bf16): a launch of
+ * few workgroups may split the cached rows into up to 4 parts and merge them
+ * (the exact softmax of the concatenation; only the rounding order differs).
+ *   parts           device scratch, 16-byte aligned, or NULL (no split);
+ *                   its contents are overwritten
+ *   parts_bytes     its size; with hsa_attention_split_workspace_bytes(dtype,
+ *                   n_active, heads, head_dim) - hsa_attention_workspace_bytes(
+ *                   dtype, n_active, d) bytes every split fits
+ * parts must not overlap q, o or the caches. Ignored for HSA_STEP_F32.
+ */
+int hsa_attention_core_split(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                             int32_t n_active, int64_t n_tokens, int32_t heads, int32_t head_dim,
+                             float scale, void* o, void* parts, size_t parts_bytes,
+                             hipStream_t stream);
+
+/*
  * Output projection of the active rows, scattered back to their tokens
  * (Section 2.3: everything after self-attention acts on A_i only):
  *   out[idx[j]] = o[j] Wo^T for j < n_active; other rows of out untouched.

@@ -149,6 +149,14 @@ HSA_API int hsa_attention_core(int dtype, const void* q, const void* k_cache, co
                         nullptr, 0, stream);
 }
 
+HSA_API int hsa_attention_core_split(int dtype, const void* q, const void* k_cache,
+                                     const void* v_cache, int32_t n_active, int64_t n_tokens,
+                                     int32_t heads, int32_t head_dim, float scale, void* o,
+                                     void* parts, size_t parts_bytes, hipStream_t stream) {
+  return attention_core(dtype, q, k_cache, v_cache, n_active, n_tokens, heads, head_dim, scale, o,
+                        parts_bytes > 0 ? parts : nullptr, parts ? parts_bytes : 0, stream);
+}
+
 HSA_API int hsa_out_scatter(int dtype, const void* o, const int32_t* idx, int32_t n_active,
                             int64_t n_tokens, int32_t d, const void* wo, void* out,
                             hipStream_t stream) {

@@ -55,6 +55,7 @@ def lib() -> ctypes.CDLL:
             "hsa_build_active_set_window": (ctypes.c_int, [P, I64, I32, I32, I32, I32, P, P, P, P]),
             "hsa_qkv_scatter": (ctypes.c_int, [ctypes.c_int, P, I32, P, I32, I64, I32, P, P, P, P, P, P, P]),
             "hsa_attention_core": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P]),
+            "hsa_attention_core_split": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P, S, P]),
             "hsa_out_scatter": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P, P]),
             "hsa_attention_workspace_bytes": (S, [ctypes.c_int, I32, I32]),
             "hsa_attention_split_workspace_bytes": (S, [ctypes.c_int, I32, I32, I32]),
@@ -88,6 +89,7 @@ EXPORTED = (
     "hsa_build_active_set_window",
     "hsa_qkv_scatter",
     "hsa_attention_core",
+    "hsa_attention_core_split",
     "hsa_out_scatter",
     "hsa_attention_workspace_bytes",
     "hsa_attention_split_workspace_bytes",
@@ -201,12 +203,21 @@ def hsa_qkv_scatter(x, idx, n_active: int, wq, wk, wv, q_out, k_cache, v_cache,
 
 
 def hsa_attention_core(q, k_cache, v_cache, n_active: int, heads: int, head_dim: int, scale: float,
-                       o, stream=None) -> None:
+                       o, stream=None, parts=None) -> None:
+    """Attention of the active queries; with `parts` (a device scratch,
+    uint8) the library may split the cached rows into key parts."""
     _dev(q, k_cache, v_cache, o)
     dt = _dtype(q, k_cache, v_cache, o)
-    st = lib().hsa_attention_core(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_active, k_cache.shape[0],
-                                  heads, head_dim, scale, _ptr(o), _stream(stream))
-    _check("hsa_attention_core", st)
+    if parts is None:
+        st = lib().hsa_attention_core(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_active, k_cache.shape[0],
+                                      heads, head_dim, scale, _ptr(o), _stream(stream))
+        _check("hsa_attention_core", st)
+        return
+    _dev(parts)
+    st = lib().hsa_attention_core_split(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_active, k_cache.shape[0],
+                                        heads, head_dim, scale, _ptr(o), _ptr(parts),
+                                        parts.numel() * parts.element_size(), _stream(stream))
+    _check("hsa_attention_core_split", st)
 
 
 def hsa_out_scatter(o, idx, n_active: int, wo, out, stream=None) -> None:

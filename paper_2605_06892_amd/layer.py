@@ -4,7 +4,8 @@ Strings the C ABI calls together in stream order (Section 2.3, then 2.4):
 
     hsa_build_active_set   A_i from the per-token budgets
     hsa_qkv_scatter        Q of A_i, K_hat/V_hat rows A_i overwritten
-    hsa_attention_core     active queries against all N cached rows
+    hsa_attention_core     active queries against all N cached rows (key parts
+                           with the split variant when few workgroups would run)
     hsa_out_scatter        output projection, scattered to rows A_i
     hsa_cached_euler       all tokens advanced by the shared sigma step
 
@@ -41,6 +42,7 @@ class BlockBuffers:
     n_active: torch.Tensor   # int32 [1]
     heads: int
     head_dim: int
+    parts: torch.Tensor | None = None  # uint8 scratch: key parts of the attention launches
 
     @property
     def N(self) -> int:
@@ -56,12 +58,19 @@ class BlockBuffers:
 
     @classmethod
     def allocate(cls, N: int, d: int, heads: int, head_dim: int, dtype: torch.dtype,
-                 device="cuda") -> "BlockBuffers":
+                 device="cuda", kv_parts: bool = True) -> "BlockBuffers":
+        """kv_parts adds the scratch with which bf16 attention launches of
+        few workgroups split their cached rows."""
         e = lambda *s, dt=dtype: torch.empty(*s, dtype=dt, device=device)  # noqa: E731
+        parts = None
+        if kv_parts and dtype == torch.bfloat16:
+            nb = H.hsa_attention_split_workspace_bytes(dtype, N, heads, head_dim) - \
+                H.hsa_attention_workspace_bytes(dtype, N, d)
+            parts = torch.empty(max(nb, 1), dtype=torch.uint8, device=device)
         return cls(x=e(N, d), wq=e(d, d), wk=e(d, d), wv=e(d, d), wo=e(d, d),
                    k_cache=e(N, d), v_cache=e(N, d), out=e(N, d), q=e(N, d), o=e(N, d),
                    budget=e(N, dt=torch.int32), idx=e(N, dt=torch.int32),
-                   n_active=e(1, dt=torch.int32), heads=heads, head_dim=head_dim)
+                   n_active=e(1, dt=torch.int32), heads=heads, head_dim=head_dim, parts=parts)
 
 
 def window_margin(center_percent: int, T: int) -> int:
@@ -83,7 +92,7 @@ def qkv(b: BlockBuffers, n_active: int, x_compact: bool = False) -> None:
 
 
 def attention(b: BlockBuffers, n_active: int) -> None:
-    H.hsa_attention_core(b.q, b.k_cache, b.v_cache, n_active, b.heads, b.head_dim, b.scale, b.o)
+    H.hsa_attention_core(b.q, b.k_cache, b.v_cache, n_active, b.heads, b.head_dim, b.scale, b.o, parts=b.parts)
 
 
 def out_projection(b: BlockBuffers, n_active: int) -> None:

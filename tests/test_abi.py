@@ -133,6 +133,10 @@ def test_attention_errors(lib):
     assert f(BF16, A, None, C, 10, 100, 4, 64, 0.125, D, None) == NULL
     assert f(BF16, A, B, C, 10, 100, 4, 64, 0.125, A, None) == ALIAS   # o on top of q
     assert f(BF16, A, B, C, 10, 100, 4, 64, 0.125, B + 512, None) == ALIAS
+    s_ = lib.hsa_attention_core_split
+    assert s_(BF16, A, B, C, 10, 100, 4, 64, 0.125, D, A + 4096, 1 << 20, None) == ALIAS  # parts over q
+    assert s_(BF16, A, B, C, 10, 100, 4, 64, 0.125, D, W + 4, 1 << 20, None) == SHAPE     # misaligned
+    assert s_(BF16, A, B, C, 10, 100, 4, 96, 0.125, D, W, 1 << 20, None) == SHAPE
     g = lib.hsa_active_attention
     need = lib.hsa_attention_workspace_bytes(BF16, 10, 256)
     assert g(BF16, A, B, C, D, 10, 100, 4, 64, 0.125, E, G, None, need, None) == WORKSPACE

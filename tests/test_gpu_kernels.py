@@ -339,6 +339,27 @@ def test_attention_key_parts(parts, N, nA, heads, dh, monkeypatch):
     assert rel_inf(host(out)[idx_np], oracle.project(o, wo_np, "bf16")) <= 1e-2
 
 
+@pytest.mark.parametrize("parts", [None, "3"])
+def test_attention_core_split(parts, monkeypatch):
+    """hsa_attention_core with a key-part scratch (the launcher's choice, or
+    3 forced) matches the oracle."""
+    if parts:
+        monkeypatch.setenv("HSA_ATTN_KV_PARTS", parts)
+    N, nA, heads, dh = 3000, 200, 2, 128
+    d = heads * dh
+    rng = np.random.default_rng(21)
+    q_np, k_np, v_np = (synth.to_bf16_values(rng.standard_normal((r, d)).astype(np.float32)) for r in (nA, N, N))
+    scale = 1.0 / math.sqrt(dh)
+    nb = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh) - \
+        H.hsa_attention_workspace_bytes(torch.bfloat16, nA, d)
+    scratch = torch.empty(nb, dtype=torch.uint8, device=DEV)
+    o = torch.empty(nA, d, dtype=torch.bfloat16, device=DEV)
+    H.hsa_attention_core(to_dev(q_np, "bf16"), to_dev(k_np, "bf16"), to_dev(v_np, "bf16"), nA, heads, dh, scale, o,
+                         parts=scratch)
+    ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, scale), "bf16")
+    assert rel_inf(host(o), ref) <= TOL["bf16"]
+
+
 def test_attention_key_parts_shift_safe(monkeypatch):
     """Parts whose maxima differ by hundreds (log2 units) merge without
     overflow or underflow of the kept terms."""
