@@ -156,12 +156,12 @@ int hsa_attention_core(int dtype, const void* q, const void* k_cache, const void
  * (the exact softmax of the concatenation; only the rounding order differs).
  *   parts           device scratch, 16-byte aligned, or NULL (no split);
  *                   its contents are overwritten
- *   parts_bytes     its size; with hsa_attention_split_workspace_bytes(dtype,
+ *   parts_bytes     its size; with hsa_attention_parts_workspace_bytes(dtype,
  *                   n_active, heads, head_dim) - hsa_attention_workspace_bytes(
  *                   dtype, n_active, d) bytes every split fits
  * parts must not overlap q, o or the caches. Ignored for HSA_STEP_F32.
  */
-int hsa_attention_core_split(int dtype, const void* q, const void* k_cache, const void* v_cache,
+int hsa_attention_core_parts(int dtype, const void* q, const void* k_cache, const void* v_cache,
                              int32_t n_active, int64_t n_tokens, int32_t heads, int32_t head_dim,
                              float scale, void* o, void* parts, size_t parts_bytes,
                              hipStream_t stream);
@@ -188,7 +188,7 @@ size_t hsa_attention_workspace_bytes(int dtype, int32_t n_active, int32_t d);
  * few workgroups: few heads or few active rows) and merges the parts in a
  * second kernel, an exact rearrangement of the softmax sum. For HSA_STEP_F32
  * this equals hsa_attention_workspace_bytes. 0 for invalid sizes. */
-size_t hsa_attention_split_workspace_bytes(int dtype, int32_t n_active, int32_t heads,
+size_t hsa_attention_parts_workspace_bytes(int dtype, int32_t n_active, int32_t heads,
                                            int32_t head_dim);
 
 /*
@@ -202,7 +202,7 @@ size_t hsa_attention_split_workspace_bytes(int dtype, int32_t n_active, int32_t 
  *                   owned by the caller; its contents are overwritten. For
  *                   bf16, the bytes past the compact tensor (from the next
  *                   256-byte boundary) may hold key parts; with
- *                   hsa_attention_split_workspace_bytes bytes every split the
+ *                   hsa_attention_parts_workspace_bytes bytes every split the
  *                   library chooses fits, with fewer it may split less.
  * out must not overlap q, the caches, wo or the workspace.
  */
@@ -434,7 +434,7 @@ typedef struct hsa_stack {
   void* k_tail;                   /* scratch [N - n_cached, d] dtype shared by the layers */
   void* v_tail;
   /* optional scratch for key parts of the bf16 attention launches (NULL: no split); with
-     hsa_attention_split_workspace_bytes(dtype, N, heads, head_dim) bytes every split fits */
+     hsa_attention_parts_workspace_bytes(dtype, N, heads, head_dim) bytes every split fits */
   void* attn_parts;
   int64_t attn_parts_bytes;
 } hsa_stack;

@@ -149,7 +149,7 @@ HSA_API int hsa_attention_core(int dtype, const void* q, const void* k_cache, co
                         nullptr, 0, stream);
 }
 
-HSA_API int hsa_attention_core_split(int dtype, const void* q, const void* k_cache,
+HSA_API int hsa_attention_core_parts(int dtype, const void* q, const void* k_cache,
                                      const void* v_cache, int32_t n_active, int64_t n_tokens,
                                      int32_t heads, int32_t head_dim, float scale, void* o,
                                      void* parts, size_t parts_bytes, hipStream_t stream) {
@@ -195,7 +195,7 @@ HSA_API size_t hsa_attention_workspace_bytes(int dtype, int32_t n_active, int32_
   return es * (size_t)n_active * (size_t)d;
 }
 
-HSA_API size_t hsa_attention_split_workspace_bytes(int dtype, int32_t n_active, int32_t heads,
+HSA_API size_t hsa_attention_parts_workspace_bytes(int dtype, int32_t n_active, int32_t heads,
                                                    int32_t head_dim) {
   if (heads < 0 || head_dim < 0 || (int64_t)heads * head_dim > INT32_MAX) return 0;
   const size_t base = hsa_attention_workspace_bytes(dtype, n_active, heads * head_dim);

@@ -55,10 +55,10 @@ def lib() -> ctypes.CDLL:
             "hsa_build_active_set_window": (ctypes.c_int, [P, I64, I32, I32, I32, I32, P, P, P, P]),
             "hsa_qkv_scatter": (ctypes.c_int, [ctypes.c_int, P, I32, P, I32, I64, I32, P, P, P, P, P, P, P]),
             "hsa_attention_core": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P]),
-            "hsa_attention_core_split": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P, S, P]),
+            "hsa_attention_core_parts": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P, S, P]),
             "hsa_out_scatter": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P, P]),
             "hsa_attention_workspace_bytes": (S, [ctypes.c_int, I32, I32]),
-            "hsa_attention_split_workspace_bytes": (S, [ctypes.c_int, I32, I32, I32]),
+            "hsa_attention_parts_workspace_bytes": (S, [ctypes.c_int, I32, I32, I32]),
             "hsa_active_attention": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P, S, P]),
             "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
             "hsa_gather_rows": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P]),
@@ -89,10 +89,10 @@ EXPORTED = (
     "hsa_build_active_set_window",
     "hsa_qkv_scatter",
     "hsa_attention_core",
-    "hsa_attention_core_split",
+    "hsa_attention_core_parts",
     "hsa_out_scatter",
     "hsa_attention_workspace_bytes",
-    "hsa_attention_split_workspace_bytes",
+    "hsa_attention_parts_workspace_bytes",
     "hsa_active_attention",
     "hsa_cached_euler",
     "hsa_gather_rows",
@@ -214,10 +214,10 @@ def hsa_attention_core(q, k_cache, v_cache, n_active: int, heads: int, head_dim:
         _check("hsa_attention_core", st)
         return
     _dev(parts)
-    st = lib().hsa_attention_core_split(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_active, k_cache.shape[0],
+    st = lib().hsa_attention_core_parts(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_active, k_cache.shape[0],
                                         heads, head_dim, scale, _ptr(o), _ptr(parts),
                                         parts.numel() * parts.element_size(), _stream(stream))
-    _check("hsa_attention_core_split", st)
+    _check("hsa_attention_core_parts", st)
 
 
 def hsa_out_scatter(o, idx, n_active: int, wo, out, stream=None) -> None:
@@ -233,8 +233,8 @@ def hsa_attention_workspace_bytes(dtype: torch.dtype, n_active: int, d: int) -> 
     return int(lib().hsa_attention_workspace_bytes(_dtype(torch.empty(0, dtype=dtype)), n_active, d))
 
 
-def hsa_attention_split_workspace_bytes(dtype: torch.dtype, n_active: int, heads: int, head_dim: int) -> int:
-    return int(lib().hsa_attention_split_workspace_bytes(_dtype(torch.empty(0, dtype=dtype)), n_active, heads,
+def hsa_attention_parts_workspace_bytes(dtype: torch.dtype, n_active: int, heads: int, head_dim: int) -> int:
+    return int(lib().hsa_attention_parts_workspace_bytes(_dtype(torch.empty(0, dtype=dtype)), n_active, heads,
                                                           head_dim))
 
 

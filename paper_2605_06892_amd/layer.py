@@ -64,7 +64,7 @@ class BlockBuffers:
         e = lambda *s, dt=dtype: torch.empty(*s, dtype=dt, device=device)  # noqa: E731
         parts = None
         if kv_parts and dtype == torch.bfloat16:
-            nb = H.hsa_attention_split_workspace_bytes(dtype, N, heads, head_dim) - \
+            nb = H.hsa_attention_parts_workspace_bytes(dtype, N, heads, head_dim) - \
                 H.hsa_attention_workspace_bytes(dtype, N, d)
             parts = torch.empty(max(nb, 1), dtype=torch.uint8, device=device)
         return cls(x=e(N, d), wq=e(d, d), wk=e(d, d), wv=e(d, d), wo=e(d, d),

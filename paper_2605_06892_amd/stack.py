@@ -79,7 +79,7 @@ class StackBuffers:
         rows = N if n_cached is None else n_cached
         parts = None
         if kv_parts and dtype == torch.bfloat16:
-            nb = H.hsa_attention_split_workspace_bytes(dtype, N, heads, head_dim) - \
+            nb = H.hsa_attention_parts_workspace_bytes(dtype, N, heads, head_dim) - \
                 H.hsa_attention_workspace_bytes(dtype, N, d)
             parts = torch.empty(max(nb, 1), dtype=torch.uint8, device=device)
         tail = None if n_cached is None else N - n_cached

@@ -75,12 +75,12 @@ def test_workspace_bytes(lib):
     assert lib.hsa_attention_workspace_bytes(BF16, -1, 256) == 0
     # the compact tensor from a 256-byte boundary, then 4 parts of fp32 (O, m, l)
     base = 8190 * 1536 * 2
-    assert lib.hsa_attention_split_workspace_bytes(BF16, 8190, 12, 128) == \
+    assert lib.hsa_attention_parts_workspace_bytes(BF16, 8190, 12, 128) == \
         (base + 255) // 256 * 256 + 4 * 8190 * 12 * (128 + 2) * 4
-    assert lib.hsa_attention_split_workspace_bytes(BF16, 10, 1, 64) == 1280 + 4 * 10 * 66 * 4
-    assert lib.hsa_attention_split_workspace_bytes(F32, 10, 4, 64) == 10 * 256 * 4
-    assert lib.hsa_attention_split_workspace_bytes(BF16, -1, 4, 64) == 0
-    assert lib.hsa_attention_split_workspace_bytes(BF16, 10, -4, 64) == 0
+    assert lib.hsa_attention_parts_workspace_bytes(BF16, 10, 1, 64) == 1280 + 4 * 10 * 66 * 4
+    assert lib.hsa_attention_parts_workspace_bytes(F32, 10, 4, 64) == 10 * 256 * 4
+    assert lib.hsa_attention_parts_workspace_bytes(BF16, -1, 4, 64) == 0
+    assert lib.hsa_attention_parts_workspace_bytes(BF16, 10, -4, 64) == 0
 
 
 def test_build_active_set_errors(lib):
@@ -133,7 +133,7 @@ def test_attention_errors(lib):
     assert f(BF16, A, None, C, 10, 100, 4, 64, 0.125, D, None) == NULL
     assert f(BF16, A, B, C, 10, 100, 4, 64, 0.125, A, None) == ALIAS   # o on top of q
     assert f(BF16, A, B, C, 10, 100, 4, 64, 0.125, B + 512, None) == ALIAS
-    s_ = lib.hsa_attention_core_split
+    s_ = lib.hsa_attention_core_parts
     assert s_(BF16, A, B, C, 10, 100, 4, 64, 0.125, D, A + 4096, 1 << 20, None) == ALIAS  # parts over q
     assert s_(BF16, A, B, C, 10, 100, 4, 64, 0.125, D, W + 4, 1 << 20, None) == SHAPE     # misaligned
     assert s_(BF16, A, B, C, 10, 100, 4, 96, 0.125, D, W, 1 << 20, None) == SHAPE

@@ -330,7 +330,7 @@ def test_attention_key_parts(parts, N, nA, heads, dh, monkeypatch):
     out0 = synth.to_bf16_values(rng.standard_normal((N, d)).astype(np.float32))
     idx_np = np.sort(rng.choice(N, nA, replace=False))
     scale = 1.0 / math.sqrt(dh)
-    ws_bytes = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh)
+    ws_bytes = H.hsa_attention_parts_workspace_bytes(torch.bfloat16, nA, heads, dh)
     o, out = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, scale, ws_bytes)
     ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, scale), "bf16")
     assert rel_inf(o, ref) <= TOL["bf16"]
@@ -340,7 +340,7 @@ def test_attention_key_parts(parts, N, nA, heads, dh, monkeypatch):
 
 
 @pytest.mark.parametrize("parts", [None, "3"])
-def test_attention_core_split(parts, monkeypatch):
+def test_attention_core_parts(parts, monkeypatch):
     """hsa_attention_core with a key-part scratch (the launcher's choice, or
     3 forced) matches the oracle."""
     if parts:
@@ -350,7 +350,7 @@ def test_attention_core_split(parts, monkeypatch):
     rng = np.random.default_rng(21)
     q_np, k_np, v_np = (synth.to_bf16_values(rng.standard_normal((r, d)).astype(np.float32)) for r in (nA, N, N))
     scale = 1.0 / math.sqrt(dh)
-    nb = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh) - \
+    nb = H.hsa_attention_parts_workspace_bytes(torch.bfloat16, nA, heads, dh) - \
         H.hsa_attention_workspace_bytes(torch.bfloat16, nA, d)
     scratch = torch.empty(nb, dtype=torch.uint8, device=DEV)
     o = torch.empty(nA, d, dtype=torch.bfloat16, device=DEV)
@@ -374,7 +374,7 @@ def test_attention_key_parts_shift_safe(monkeypatch):
     wo_np = synth.to_bf16_values(np.eye(dh, dtype=np.float32))
     idx_np = np.arange(nA)
     out0 = np.zeros((N, dh), np.float32)
-    ws_bytes = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh)
+    ws_bytes = H.hsa_attention_parts_workspace_bytes(torch.bfloat16, nA, heads, dh)
     o, _ = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, 1.0, ws_bytes)
     ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, 1.0), "bf16")
     assert np.all(np.isfinite(o))
@@ -383,7 +383,7 @@ def test_attention_key_parts_shift_safe(monkeypatch):
 
 def test_attention_key_parts_auto_and_minimum_workspace():
     """A launch of few workgroups (one head, 256 queries, 4096 keys) splits
-    on its own with the split workspace and matches the oracle; with the
+    on its own with the key-part workspace and matches the oracle; with the
     minimum workspace it does not split and equals hsa_attention_core bit for
     bit."""
     N, nA, heads, dh = 4096, 256, 1, 128
@@ -394,7 +394,7 @@ def test_attention_key_parts_auto_and_minimum_workspace():
     idx_np = np.arange(nA)
     scale = 1.0 / math.sqrt(dh)
     ref = oracle.round_to(oracle.attention(q_np, k_np, v_np, heads, dh, scale), "bf16")
-    split = H.hsa_attention_split_workspace_bytes(torch.bfloat16, nA, heads, dh)
+    split = H.hsa_attention_parts_workspace_bytes(torch.bfloat16, nA, heads, dh)
     o_split, _ = _active_attention_with_parts(q_np, k_np, v_np, wo_np, out0, idx_np, heads, dh, scale, split)
     assert rel_inf(o_split, ref) <= TOL["bf16"]
     minimum = H.hsa_attention_workspace_bytes(torch.bfloat16, nA, heads * dh)
