@@ -50,8 +50,8 @@ ATTN_SRC = os.path.join(ROOT, "paper_2605_06892_amd", "csrc", "attention_bf16.hi
 def parse():
     p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="wan14b", choices=["wan14b", "wan1.3b", "wan14b_720p"])
     p.add_argument("--iteration", type=int, default=1, help="timed iteration (1: 25%% active)")
     p.add_argument("--second-iteration", type=int, default=2, help="also time this iteration (-1: skip)")
