@@ -255,58 +255,88 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   for (; k + 2 * STAGES - 1 <= nk; k += STAGES) round(k, STAGES, std::true_type{});
   for (; k < nk; k += STAGES) round(k, min(STAGES, nk - k), std::false_type{});
 
-  // acc[i][j][e]: output row m = tile row + i*32 + l32,
-  //               column n = tile col + j*32 + (e/4)*8 + hi*4 + e%4
+  // Epilogue through LDS. acc[i][j][e] is output row (tile row + i*32 + l32),
+  // column (tile col + j*32 + (e/4)*8 + hi*4 + e%4): a lane holds 4 columns
+  // of one row, so direct stores would write 16-byte pieces of 32 rows per
+  // instruction. Instead, for each 32-row block i, every wave writes its
+  // fp32 values (row scale, RoPE and GELU applied) to its own LDS region,
+  // then reads them back row-contiguous and stores runs of 4 columns per
+  // lane, 128 bytes or more per row (the residual is added there, then the
+  // value rounded once). Waves 0-3 use the first stage's array, 4-7 the
+  // second; the scatter target of each row travels through LDS too.
+  constexpr int TNP = TN + 4;         // padded staging row, floats
+  constexpr int QPR = TN / 4;         // 4-column groups per row
+  constexpr int REGION = 32 * TNP * 4 + 32 * 8 + 32 * 4;
+  static_assert(4 * REGION <= TL::STAGE * 2, "epilogue staging must fit in a stage");
+  __syncthreads();  // every wave is done with the stages
+  char* region = reinterpret_cast<char*>((wave < 4) ? L0 : L1) + (wave % 4) * REGION;
+  float* blk = reinterpret_cast<float*>(region);
+  long* row_off = reinterpret_cast<long*>(region + 32 * TNP * 4);   // output element offset
+  int* row_buf = reinterpret_cast<int*>(region + 32 * TNP * 4 + 32 * 8);  // 0: C, 1: C2, -1: none
   const int32_t* c_rows = oz.c_rows;
+  const bool rope = g.rope_cs && ((g.rope_outs >> z) & 1);
+  const int col0 = tn * BN + wn * TN;  // first output column of the wave tile
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int m = tm * BM + wm * TM + i * 32 + l32;
-    if (m >= g.M) continue;
-    const int crow = c_rows ? c_rows[m] : m;
-    if (crow < 0 || crow >= oz.c_limit) continue;
-    void* cbase = oz.C;
-    long orow = crow;
-    if (oz.C2 && crow >= oz.c_split) {  // rows past the split go to the second buffer
-      cbase = oz.C2;
-      orow = crow - oz.c_split;
+    int buf = -1;
+    long obase = 0;
+    if (m < g.M) {
+      const int crow = c_rows ? c_rows[m] : m;
+      if (crow >= 0 && crow < oz.c_limit) {
+        const bool second = oz.C2 && crow >= oz.c_split;  // rows past the split go to C2
+        buf = second ? 1 : 0;
+        obase = (long)(second ? crow - oz.c_split : crow) * g.ldc;
+      }
     }
-    const long obase = orow * g.ldc;
-    const float rs = g.row_scale ? g.row_scale[m] : 1.f;
-    const bool rope = g.rope_cs && ((g.rope_outs >> z) & 1);
+    if (hi == 0) {
+      row_off[l32] = obase;
+      row_buf[l32] = buf;
+    }
+    const float rs = (g.row_scale && m < g.M) ? g.row_scale[m] : 1.f;
     RopeRow rr{0, 0, 0};
-    if (rope) rr = rope_row(g, m);
+    if (rope && buf >= 0) rr = rope_row(g, m);
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int n = tn * BN + wn * TN + j * 32 + q * 8 + hi * 4;
-        if (n < g.Nc) {
-          f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                     acc[i][j][4 * q + 3]};
-          if (g.row_scale) v *= rs;
-          if (rope) {
-            const int k = (n % g.rope_dh) >> 1;
-            const f32x2 r0 = rope_pair(g, rr, k, v[0], v[1]);
-            const f32x2 r1 = rope_pair(g, rr, k + 1, v[2], v[3]);
-            v = (f32x4){r0[0], r0[1], r1[0], r1[1]};
-          }
-          if constexpr (EPI == kEpiF32) {
-            *reinterpret_cast<f32x4*>(static_cast<float*>(cbase) + obase + n) = v;
-          } else {
-            if constexpr (EPI == kEpiBf16Residual) {
-              const bf16x4 r =
-                  *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + obase + n);
-              v += __builtin_convertvector(r, f32x4);
-            }
-            if constexpr (EPI == kEpiBf16Gelu) {
-#pragma unroll
-              for (int u = 0; u < 4; ++u) v[u] = gelu_tanh(v[u]);
-            }
-            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(cbase) + obase + n) = to_bf16x4(v);
-          }
+        const int c = j * 32 + q * 8 + hi * 4;
+        f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (g.row_scale) v *= rs;
+        if (rope && buf >= 0 && col0 + c < g.Nc) {
+          const int k = ((col0 + c) % g.rope_dh) >> 1;
+          const f32x2 r0 = rope_pair(g, rr, k, v[0], v[1]);
+          const f32x2 r1 = rope_pair(g, rr, k + 1, v[2], v[3]);
+          v = (f32x4){r0[0], r0[1], r1[0], r1[1]};
         }
+        if constexpr (EPI == kEpiBf16Gelu) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] = gelu_tanh(v[u]);
+        }
+        *reinterpret_cast<f32x4*>(blk + l32 * TNP + c) = v;
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    // row-contiguous read-back: 4 columns per lane, QPR lanes per row
+#pragma unroll
+    for (int f = lane; f < 32 * QPR; f += 64) {
+      const int r = f / QPR, cq = f - r * QPR;
+      const int rb = row_buf[r];
+      const int n = col0 + cq * 4;
+      if (rb < 0 || n >= g.Nc) continue;
+      f32x4 v = *reinterpret_cast<const f32x4*>(blk + r * TNP + cq * 4);
+      void* cbase = rb ? oz.C2 : oz.C;
+      const long o = row_off[r] + n;
+      if constexpr (EPI == kEpiF32) {
+        *reinterpret_cast<f32x4*>(static_cast<float*>(cbase) + o) = v;
+      } else {
+        if constexpr (EPI == kEpiBf16Residual)
+          v += __builtin_convertvector(*reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + o),
+                                       f32x4);
+        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(cbase) + o) = to_bf16x4(v);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // reads done before the next block's writes
   }
 }
 
