@@ -268,6 +268,7 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   constexpr int QPR = TN / 4;         // 4-column groups per row
   constexpr int REGION = 32 * TNP * 4 + 32 * 8 + 32 * 4;
   static_assert(4 * REGION <= TL::STAGE * 2, "epilogue staging must fit in a stage");
+  static_assert(QPR % 2 == 0, "the wave covers whole rows in each read-back pass");
   __syncthreads();  // every wave is done with the stages
   char* region = reinterpret_cast<char*>((wave < 4) ? L0 : L1) + (wave % 4) * REGION;
   float* blk = reinterpret_cast<float*>(region);
@@ -317,9 +318,11 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    // row-contiguous read-back: 4 columns per lane, QPR lanes per row
+    // row-contiguous read-back: 4 columns per lane, QPR lanes per row, QPR/2
+    // passes of the wave
 #pragma unroll
-    for (int f = lane; f < 32 * QPR; f += 64) {
+    for (int t = 0; t < QPR / 2; ++t) {
+      const int f = lane + 64 * t;
       const int r = f / QPR, cq = f - r * QPR;
       const int rb = row_buf[r];
       const int n = col0 + cq * 4;
