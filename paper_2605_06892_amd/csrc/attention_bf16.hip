@@ -12,18 +12,19 @@
 // workspace) and attention_combine merges the parts, rescaling each by
 // 2^(m_p - max m) (the softmax of a concatenation).
 //
-// K/V tiles of 64 cached rows go global -> LDS directly (global_load_lds_dwordx4:
+// K/V tiles of 96 cached rows go global -> LDS directly (global_load_lds_dwordx4:
 // each wave instruction fills one contiguous 1 KB segment of LDS, lane l at
-// byte 16*l), three tiles deep, issued two tiles ahead by one wave per SIMD,
-// one barrier per tile.
+// byte 16*l), three tiles deep (144 KB of LDS at 128-wide heads), issued two
+// tiles ahead by one wave per SIMD, one barrier per tile (every three 32-key
+// blocks).
 // Rows are stored unpadded with the 16-byte chunks of each row permuted by an
 // XOR with a function of the row (K: f(r) = ((r&3)<<2)|((r>>2)&3) for 128-wide
 // heads; V: f(r) = (r&3)<<2), so that the K fragment reads (16 rows, one chunk)
 // and the V transpose reads (4 rows, 4 chunks) both hit disjoint LDS banks.
 // Rows beyond N are loaded from row N-1 and masked out of the softmax. The N
-// rows may come in two segments: a cache prefix and, from row n_split on (a
-// multiple of the 64-row tile), fresh rows of a second buffer (the
-// prefix-only cache of reordered tokens).
+// rows may come in two segments: a cache prefix and, from row n_split on,
+// fresh rows of a second buffer (the prefix-only cache of reordered tokens);
+// a tile across n_split picks the segment per row.
 //
 // Keys are consumed in 32-row blocks. Per block:
 //   S^T = K Q^T - m   v_mfma_f32_32x32x16_bf16 with K rows as the A operand
@@ -58,7 +59,7 @@
 namespace hsa {
 namespace {
 
-constexpr int BKV = 64;                 // cached rows per LDS tile
+constexpr int BKV = 96;                 // cached rows per LDS tile (three 32-key blocks)
 constexpr int NBUF = 3;                 // LDS tiles in flight
 constexpr float kSlowSum = 65536.0f;    // 2^16: raise the reference maximum
 
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   const int h = hp / parts;
   const int part = hp - h * parts;
   // cached rows of this part (all of them when parts == 1); kv_chunk is a
-  // multiple of the tile, so tiles never straddle a part or the segment split
+  // multiple of the tile, so tiles never straddle a part
   const int kv_begin = part * kv_chunk;
   const int kv_end = min(n_kv, kv_begin + kv_chunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -166,13 +167,13 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     if (wave >= LW) return;
     bf16* kd = kbuf(buf) + wave * 512;
     bf16* vd = vbuf(buf) + wave * 512;
-    // segment of this tile (a tile never straddles the split: n_split is a
-    // multiple of BKV), chosen once per tile
+    // segment of the tile when all of its rows exist and lie on one side of
+    // the split, chosen once per tile
     const bool tail = SPLIT && kv0 >= n_split;
     const bf16* kb = tail ? kg2 : kg;
     const bf16* vb = tail ? vg2 : vg;
     const long off = tail ? (long)n_split : 0;
-    if (kv0 + BKV <= n_kv) {  // uniform: every row of the tile exists
+    if (kv0 + BKV <= n_kv && (!SPLIT || tail || kv0 + BKV <= n_split)) {
       const bf16* ks = kb + (kv0 + r0 - off) * d;
       const bf16* vs = vb + (kv0 + r0 - off) * d;
 #pragma unroll
@@ -182,13 +183,16 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
         __builtin_amdgcn_global_load_lds((global_cvoid*)(vs + (long)i * RSTEP * d + vch(i)),
                                          (lds_void*)(vd + i * LW * 512), 16, 0, 0);
       }
-    } else {  // the last, ragged tile: rows past N are read from row N-1
+    } else {  // the last, ragged tile (rows past N are read from row N-1) or a
+              // tile across the split: segment and row chosen per row
 #pragma unroll
       for (int i = 0; i < LL; ++i) {
-        const long n = min(kv0 + r0 + i * RSTEP, n_kv - 1) - off;
-        __builtin_amdgcn_global_load_lds((global_cvoid*)(kb + n * d + kch(i)),
+        const int n = min(kv0 + r0 + i * RSTEP, n_kv - 1);
+        const bool t = SPLIT && n >= n_split;
+        const long row = t ? n - n_split : n;
+        __builtin_amdgcn_global_load_lds((global_cvoid*)((t ? kg2 : kg) + row * d + kch(i)),
                                          (lds_void*)(kd + i * LW * 512), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((global_cvoid*)(vb + n * d + vch(i)),
+        __builtin_amdgcn_global_load_lds((global_cvoid*)((t ? vg2 : vg) + row * d + vch(i)),
                                          (lds_void*)(vd + i * LW * 512), 16, 0, 0);
       }
     }
@@ -304,22 +308,29 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   scores(B0{}, 0, sa);
   // tile it lives in buffer it % 3; the loop is unrolled by 3 so that every
   // buffer index is a compile-time constant
-  auto tile = [&](auto buf, auto nxt, auto nn, int it) {
+  // s0 holds the scores of the tile's block 0 on entry; the three steps
+  // alternate the two score registers, so the next tile starts from s1
+  auto tile = [&](auto buf, auto nxt, auto nn, int it, f32x16& s0, f32x16& s1) {
     const int kv0 = kv_begin + it * BKV;
     // block 0 of this tile; the next block is block 1 of the same tile
-    step(sa, sb, buf, 32, buf, 0, kv0);
-    // tile it+1 (issued one iteration ago) has landed; after this barrier every
+    step(s0, s1, buf, 32, buf, 0, kv0);
+    // tile it+1 (issued one tile ago) has landed; after this barrier every
     // wave is done with tile it-1, whose buffer receives tile it+2
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
     if (it + 2 < n_tiles) issue_tile(nn, kv0 + 2 * BKV);
-    // block 1 of this tile; the next block is block 0 of tile it+1
-    if (kv0 + 32 < kv_end) step(sb, sa, nxt, 0, buf, 32, kv0 + 32);
+    // block 1; the next block is block 2 of the same tile
+    if (kv0 + 32 < kv_end) step(s1, s0, buf, 64, buf, 32, kv0 + 32);
+    // block 2; the next block is block 0 of tile it+1
+    if (kv0 + 64 < kv_end) step(s0, s1, nxt, 0, buf, 64, kv0 + 64);
   };
   for (int it = 0; it < n_tiles; it += NBUF) {
-    tile(B0{}, B1{}, B2{}, it);
-    if (it + 1 < n_tiles) tile(B1{}, B2{}, B0{}, it + 1);
-    if (it + 2 < n_tiles) tile(B2{}, B0{}, B1{}, it + 2);
+    tile(B0{}, B1{}, B2{}, it, sa, sb);
+    if (it + 1 < n_tiles) tile(B1{}, B2{}, B0{}, it + 1, sb, sa);
+    if (it + 2 < n_tiles) tile(B2{}, B0{}, B1{}, it + 2, sa, sb);
+    const f32x16 t = sa;  // three tiles of three steps: the roles swap
+    sa = sb;
+    sb = t;
   }
 
   // acc[dt][e]: channel dt*32 + (e/4)*8 + hi*4 + e%4 of query l32
@@ -417,10 +428,8 @@ template <int DH, int NW>
 hipError_t launch_cfg(const void* q, const void* k, const void* v, void* o, int n_q, int n_kv,
                       int heads, float sl2e, hipStream_t s, const void* k2, const void* v2,
                       int n_split, const KvParts& kp) {
-  if (n_split < n_kv) {
-    if (n_split % BKV != 0) return hipErrorInvalidValue;
+  if (n_split < n_kv)
     return launch_split<DH, NW, true>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
-  }
   return launch_split<DH, NW, false>(q, k, v, o, n_q, n_kv, heads, sl2e, s, k2, v2, n_split, kp);
 }
 

@@ -148,7 +148,7 @@ def reorder(b: StackBuffers, T: int) -> torch.Tensor:
 
 def prefix_rows(n_lead: int, N: int) -> int:
     """Cache rows of the prefix-only cache for n_lead non-baseline tokens: the
-    next multiple of the 64-row attention tile (at most N)."""
+    next multiple of 64, the granularity the stack accepts (at most N)."""
     return min(N, -(-n_lead // 64) * 64)
 
 

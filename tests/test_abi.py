@@ -380,7 +380,7 @@ def test_prefix_cache_stack_errors(lib):
     assert call(_stack(prefix_cache=1, n_cached=512)[0], g=2) == BUDGET   # fixed groups only
     assert call(_stack(prefix_cache=1, n_cached=1001)[0]) == SHAPE
     assert call(_stack(prefix_cache=1, n_cached=-1)[0]) == SHAPE
-    assert call(_stack(prefix_cache=1, n_cached=500)[0]) == SHAPE        # not a multiple of the key tile
+    assert call(_stack(prefix_cache=1, n_cached=500)[0]) == SHAPE        # not a multiple of 64
     assert call(_stack(prefix_cache=2, n_cached=512)[0]) == SHAPE
     assert call(_stack(prefix_cache=1, n_cached=512)[0]) == NULL         # tails missing
     assert call(_stack(reserved3=1)[0]) == SHAPE

@@ -500,15 +500,17 @@ def test_tiny_prefix_cache_trajectory():
     assert rel_inf(host(S.restore_order(b, perm)), base[-1]["x"]) <= TOL["f32"]
 
 
-@pytest.mark.parametrize("kv_parts", [None, "4"])
-def test_prefix_cache_equals_full_cache_bitwise(kv_parts, monkeypatch):
+@pytest.mark.parametrize("kv_parts,extra", [(None, 0), ("4", 0), (None, 64)])
+def test_prefix_cache_equals_full_cache_bitwise(kv_parts, extra, monkeypatch):
     """At the Wan-1.3B shape (3 layers, RoPE, HSA-75A groups with a 25%
     baseline group reordered to the end) the prefix-only cache changes only
     where the baseline rows' keys live: latents, velocities and the cached
     prefix rows are bit-identical to the full-cache run. The 25%-active
     iteration splits its attention keys (2 parts by the launcher's choice,
     or 4 forced), so parts that span the cache prefix and the fresh tail
-    are covered too."""
+    are covered too. The smallest prefix is 24576 rows, a whole number of
+    96-row key tiles; with 64 more cached rows (baseline tokens kept in the
+    prefix) one key tile spans the prefix and the fresh tail."""
     if kv_parts:
         monkeypatch.setenv("HSA_ATTN_KV_PARTS", kv_parts)
     wl = synth.WORKLOADS["wan1.3b_stack"]
@@ -518,7 +520,7 @@ def test_prefix_cache_equals_full_cache_bitwise(kv_parts, monkeypatch):
     budget = synth.random_budgets(N, groups, seed=8)
     sig = synth.linear_sigmas(wl.T)
     runs = []
-    for n_cached in (None, S.prefix_rows(int(np.sum(budget < wl.T)), N)):
+    for n_cached in (None, S.prefix_rows(int(np.sum(budget < wl.T)), N) + extra):
         b = S.StackBuffers.allocate(N, wl.euler_channels, L, wl.heads, wl.dh, torch.bfloat16, n_cached=n_cached)
         src = _upload(wl, wts, N, L) if not runs else runs[0][0]
         if runs:
