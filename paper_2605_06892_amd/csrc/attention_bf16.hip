@@ -123,7 +123,8 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   // multiple of the tile, so tiles never straddle a part
   const int kv_begin = part * kv_chunk;
   const int kv_end = min(n_kv, kv_begin + kv_chunk);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar
   const int l32 = lane & 31, hi = lane >> 5;
   const long col0 = (long)h * DH;
 
@@ -163,6 +164,9 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   // is a multiple of the permutation's period, 16 rows)
   auto kch = [&](int i) { return (slot ^ swz_k<DH>(r0 + i * RSTEP)) * 8; };
   auto vch = [&](int i) { return (slot ^ swz_v<DH>(r0 + i * RSTEP)) * 8; };
+  static_assert(RSTEP % 16 == 0, "one chunk permutation for all of a loader's rows");
+  const uint32_t k_lane = (uint32_t)(r0 * d + kch(0)) * 2;  // bytes from the tile's first row
+  const uint32_t v_lane = (uint32_t)(r0 * d + vch(0)) * 2;
   auto issue_tile = [&](auto buf, int kv0) {
     if (wave >= LW) return;
     bf16* kd = kbuf(buf) + wave * 512;
@@ -174,13 +178,14 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     const bf16* vb = tail ? vg2 : vg;
     const long off = tail ? (long)n_split : 0;
     if (kv0 + BKV <= n_kv && (!SPLIT || tail || kv0 + BKV <= n_split)) {
-      const bf16* ks = kb + (kv0 + r0 - off) * d;
-      const bf16* vs = vb + (kv0 + r0 - off) * d;
+      // uniform tile base (scalar) + the lane's 32-bit byte offset
+      const char* ks = reinterpret_cast<const char*>(kb + (long)(kv0 - off) * d);
+      const char* vs = reinterpret_cast<const char*>(vb + (long)(kv0 - off) * d);
 #pragma unroll
       for (int i = 0; i < LL; ++i) {
-        __builtin_amdgcn_global_load_lds((global_cvoid*)(ks + (long)i * RSTEP * d + kch(i)),
+        __builtin_amdgcn_global_load_lds((global_cvoid*)(ks + (long)i * RSTEP * d * 2 + k_lane),
                                          (lds_void*)(kd + i * LW * 512), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((global_cvoid*)(vs + (long)i * RSTEP * d + vch(i)),
+        __builtin_amdgcn_global_load_lds((global_cvoid*)(vs + (long)i * RSTEP * d * 2 + v_lane),
                                          (lds_void*)(vd + i * LW * 512), 16, 0, 0);
       }
     } else {  // the last, ragged tile (rows past N are read from row N-1) or a
