@@ -58,7 +58,8 @@ def parse():
     p.add_argument("--layout", default="scattered", choices=["scattered", "contiguous"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-schedules", action="store_true", help="skip the preset-schedule trajectories")
-    p.add_argument("--no-euler-stress", action="store_true", help="skip the Euler bandwidth-stress shape")
+    p.add_argument("--no-euler-stress", action="store_true",
+                   help="skip the Euler and gather bandwidth-stress shapes")
     p.add_argument("--no-extra-timings", action="store_true",
                    help="skip the 100%%-active, cold-cache and other-layout timings of the step")
     p.add_argument("--no-end-to-end", action="store_true",
@@ -71,8 +72,9 @@ def parse():
     p.add_argument("--write-traffic", metavar="DIR", default=None,
                    help="from counter passes DIR/{attn,copy}_{fetch,write} write the attention HBM traffic file")
     p.add_argument("--only", default=None,
-                   choices=["active_set", "qkv", "attention", "out", "euler", "copy"],
-                   help="launch only this kernel --steps times after setup (profiling passes)")
+                   choices=["active_set", "qkv", "attention", "out", "euler", "copy", "stress"],
+                   help="launch only this kernel --steps times after setup (profiling passes); "
+                        "stress: only the gather and Euler bandwidth-stress shapes")
     return p.parse_args()
 
 
@@ -352,6 +354,36 @@ def euler_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
             "bytes": nbytes, "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def gather_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
+    """The index-driven row gather of the stack's latent (hsa_gather_rows) at the
+    same bandwidth-stress shape: every 4th of 16M fp32 rows of 16 channels
+    gathered into compact bf16 rows. HBM bytes per launch (the index, the rows
+    read, the compact rows written) over its event time, against the HBM peak."""
+    import torch
+
+    from paper_2605_06892_amd import hsa_step as H
+
+    x = torch.ones(n_tokens, channels, device=dev)
+    idx = torch.arange(0, n_tokens, 4, dtype=torch.int32, device=dev)
+    na = idx.numel()
+    xa = torch.empty(na, channels, device=dev, dtype=torch.bfloat16)
+    ts = []
+    for r in range(reps + 2):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        H.hsa_gather_rows(x, idx, na, xa)
+        b.record()
+        torch.cuda.synchronize()
+        if r >= 2:
+            ts.append(a.elapsed_time(b))
+    ms = float(np.median(ts))
+    nbytes = na * (4 + channels * 4 + channels * 2)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del x, idx, xa
+    return {"tokens": n_tokens, "channels": channels, "rows": na, "ms": round(ms, 4), "bytes": nbytes,
+            "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def stack_flops(n_active, N, d, C, layers, ffn=0, ctx=0):
     """Matrix-product FLOPs of one stack pass over n_active rows: embedding,
     per layer Q/K/V, attention against N cached rows and the output
@@ -568,6 +600,9 @@ def main():
             out["end_to_end_blocks"] = end_to_end(dev, "wan1.3b_blocks", presets=True, rope=True)
         print(json.dumps(out))
         return
+    if args.only == "stress":
+        print(json.dumps({"gather_stress": gather_stress(dev), "euler_stress": euler_stress(dev)}))
+        return
     wl = synth.WORKLOADS[args.workload]
     sigmas = synth.linear_sigmas(wl.T)
     blk, budget, b, eul = setup(wl, args.layout, dev)
@@ -672,6 +707,7 @@ def main():
         b.budget.copy_(torch.from_numpy(budget))
     if not args.no_euler_stress:
         out["euler_stress"] = euler_stress(dev)
+        out["gather_stress"] = gather_stress(dev)
     if not args.no_schedules or not args.no_end_to_end:
         del b, eul
         torch.cuda.empty_cache()

@@ -42,23 +42,39 @@ int grid_for(long work) {
   return (int)g;
 }
 
+// Each thread keeps kGatherU independent 16-byte row loads in flight before
+// its stores; the latent rows are streamed once (nontemporal loads).
+constexpr int kGatherU = 4;
+
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void gather_latent_vec(const f32x4* __restrict__ x,
                                                               const int32_t* __restrict__ idx,
                                                               int n_active, long n_tokens, int vpr,
                                                               void* __restrict__ xa) {
   const long total = (long)n_active * vpr;
-  for (long e = blockIdx.x * (long)kThreads + threadIdx.x; e < total;
-       e += (long)gridDim.x * kThreads) {
-    const long j = e / vpr;
-    const int c = (int)(e - j * vpr);
-    const int t = idx[j];
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (t >= 0 && t < n_tokens) v = x[(long)t * vpr + c];
-    if constexpr (BF16)
-      static_cast<bf16x4*>(xa)[e] = to_bf16x4(v);
-    else
-      static_cast<f32x4*>(xa)[e] = v;
+  for (long e0 = blockIdx.x * (long)(kThreads * kGatherU) + threadIdx.x; e0 < total;
+       e0 += (long)gridDim.x * kThreads * kGatherU) {
+    f32x4 v[kGatherU];
+#pragma unroll
+    for (int u = 0; u < kGatherU; ++u) {
+      const long e = e0 + (long)u * kThreads;
+      v[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      if (e < total) {
+        const long j = e / vpr;
+        const int c = (int)(e - j * vpr);
+        const int t = idx[j];
+        if (t >= 0 && t < n_tokens) v[u] = __builtin_nontemporal_load(x + (long)t * vpr + c);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kGatherU; ++u) {
+      const long e = e0 + (long)u * kThreads;
+      if (e >= total) break;
+      if constexpr (BF16)
+        static_cast<bf16x4*>(xa)[e] = to_bf16x4(v[u]);
+      else
+        static_cast<f32x4*>(xa)[e] = v[u];
+    }
   }
 }
 
@@ -330,7 +346,7 @@ hipError_t launch_gather_latent(const float* x, const int32_t* idx, int n_active
                    (reinterpret_cast<uintptr_t>(xa) & (out_bf16 ? 7 : 15)) == 0;
   if (vec) {
     const int vpr = channels / 4;
-    const dim3 grid(grid_for((long)n_active * vpr));
+    const dim3 grid(grid_for(((long)n_active * vpr + kGatherU - 1) / kGatherU));
     if (out_bf16)
       hipLaunchKernelGGL(gather_latent_vec<true>, grid, dim3(kThreads), 0, s,
                          reinterpret_cast<const f32x4*>(x), idx, n_active, n_tokens, vpr, xa);
