@@ -16,7 +16,9 @@
 // step. Within a step the fragment reads of k slice s+1 and the stage loads
 // are placed one per MFMA between the MFMAs of slice s, so neither the LDS
 // latency nor the load issue stalls the matrix pipe (measured: issuing them
-// in bursts ahead of the MFMAs cost 5-10%). The 16-byte chunks of tile row r
+// in bursts ahead of the MFMAs cost 5-10%), and the MFMAs of (some of) the
+// last slice's fragment rows run behind the next step's barrier, where they
+// cover that step's first reads (1-4%). The 16-byte chunks of tile row r
 // sit at slot chunk ^ ((r >> 1) & 7), which keeps the fragment reads (16
 // rows, one chunk) on disjoint banks. Each stage is its own LDS array and the
 // K loop is unrolled by the stage count, so the compiler can tell the
@@ -166,17 +168,36 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = (f32x16){};
 
-  // compute(st, LG): the MFMAs of one stage. The reads of slice kk+1 are
-  // spread between the MFMAs of slice kk, so their latency hides behind them
-  // (only slice 0 waits for its reads), and the LG stage loads issued just
-  // before (0 or LOADS) are spread one per MFMA over the first slices, so
-  // that they do not hold the wave at their issue ahead of its MFMAs.
+  // Fragments live in two register buffers: slice kk of a stage goes to
+  // buffer kk & 1, so a stage's last slice is in buffer 1. The MFMAs of its
+  // last DEF fragment rows are deferred to the start of the next stage's
+  // compute, behind the barrier: they need registers only, and they keep the
+  // matrix pipe busy while the next stage's first fragment reads are in
+  // flight (otherwise every wave waits for them right after the barrier).
+  // DEF is all rows at two row tiles per wave and half of them at four, where
+  // more deferred fragments would not fit in 256 registers. Buffer 1 starts at
+  // zero, so the first stage's deferred MFMAs add exact zeros.
+  bf16x8 af[2][MI], bfr[2][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i) af[1][i] = (bf16x8){};
+#pragma unroll
+  for (int j = 0; j < NI; ++j) bfr[1][j] = (bf16x8){};
+  constexpr int DEF = MI <= 2 ? MI : MI / 2;
+  // the MFMAs of fragment rows i0 .. i1-1 of buffer b
+  auto mfmas = [&](auto bc, auto i0c, auto i1c) {
+    constexpr int b = decltype(bc)::value, i0 = decltype(i0c)::value, i1 = decltype(i1c)::value;
+#pragma unroll
+    for (int i = i0; i < i1; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[b][j], af[b][i], acc[i][j], 0, 0, 0);
+  };
   auto compute = [&](auto st, auto lg) {
     constexpr int LG = decltype(lg)::value, KS = BK / 16, R = MI + NI, M = MI * NI;
     static_assert(M >= R, "one MFMA per fragment read at least");
+    static_assert(KS % 2 == 0, "the last slice of a stage is in buffer 1");
     const bf16* As = stage(st) + (wm * TM + l32) * BK;
     const bf16* Bs = stage(st) + BM * BK + (wn * TN + l32) * BK;
-    bf16x8 af[2][MI], bfr[2][NI];
     auto ld = [&](int kk, int b) {
       const int off = (kk * 16) ^ xr;
 #pragma unroll
@@ -185,22 +206,32 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
       for (int j = 0; j < NI; ++j) bfr[b][j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * BK + off);
     };
     ld(0, 0);
+    // the previous stage's deferred rows, then this stage's slices 0 .. KS-2
+    // with the reads of each next slice and the stage loads between the MFMAs
+    mfmas(std::integral_constant<int, 1>{}, std::integral_constant<int, MI - DEF>{},
+          std::integral_constant<int, MI>{});
     __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
-    static_for<0, KS>([&](auto kc) {
+    static_for<0, DEF * NI>([&](auto mc) {
+      constexpr int m = decltype(mc)::value;
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if constexpr (m < LG) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    });
+    static_for<0, KS - 1>([&](auto kc) {
       constexpr int kk = decltype(kc)::value;
-      if constexpr (kk + 1 < KS) ld(kk + 1, (kk + 1) & 1);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i], acc[i][j], 0, 0, 0);
+      ld(kk + 1, (kk + 1) & 1);
+      mfmas(std::integral_constant<int, kk & 1>{}, std::integral_constant<int, 0>{},
+            std::integral_constant<int, MI>{});
       static_for<0, M>([&](auto mc) {
         constexpr int m = decltype(mc)::value;
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if constexpr (kk + 1 < KS && m < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        if constexpr (kk * M + m < LG) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        if constexpr (m < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if constexpr (DEF * NI + kk * M + m < LG) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       });
     });
+    // slice KS-1: the rows before the deferred ones
+    mfmas(std::integral_constant<int, 1>{}, std::integral_constant<int, 0>{},
+          std::integral_constant<int, MI - DEF>{});
+    static_for<0, (MI - DEF) * NI>([&](auto mc) { __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); });
   };
 
   using S0 = std::integral_constant<int, 0>;
@@ -254,6 +285,8 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   int k = 0;
   for (; k + 2 * STAGES - 1 <= nk; k += STAGES) round(k, STAGES, std::true_type{});
   for (; k < nk; k += STAGES) round(k, min(STAGES, nk - k), std::false_type{});
+  mfmas(std::integral_constant<int, 1>{}, std::integral_constant<int, MI - DEF>{},
+        std::integral_constant<int, MI>{});  // the last stage's deferred rows
 
   // Epilogue through LDS. acc[i][j][e] is output row (tile row + i*32 + l32),
   // column (tile col + j*32 + (e/4)*8 + hi*4 + e%4): a lane holds 4 columns
