@@ -165,8 +165,8 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   auto kch = [&](int i) { return (slot ^ swz_k<DH>(r0 + i * RSTEP)) * 8; };
   auto vch = [&](int i) { return (slot ^ swz_v<DH>(r0 + i * RSTEP)) * 8; };
   static_assert(RSTEP % 16 == 0, "one chunk permutation for all of a loader's rows");
-  const uint32_t k_lane = (uint32_t)(r0 * d + kch(0)) * 2;  // bytes from the tile's first row
-  const uint32_t v_lane = (uint32_t)(r0 * d + vch(0)) * 2;
+  const long k_lane = ((long)r0 * d + kch(0)) * 2;  // bytes from the tile's first row
+  const long v_lane = ((long)r0 * d + vch(0)) * 2;
   auto issue_tile = [&](auto buf, int kv0) {
     if (wave >= LW) return;
     bf16* kd = kbuf(buf) + wave * 512;
