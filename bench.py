@@ -43,6 +43,8 @@ METRIC = "HSA layer-step ms + active-attention TFLOP/s at N=32760, 25%/50% activ
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 EULER_CHANNELS = 16         # latent channels advanced by the cached Euler update
+MI355X_SIMDS = 1024         # 256 CUs x 4 SIMDs
+MI355X_XCDS = 8
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_wan14b_traffic.txt")
 ATTN_SRC = os.path.join(ROOT, "paper_2605_06892_amd", "csrc", "attention_bf16.hip")
 
@@ -232,6 +234,17 @@ def summarize(d):
         lines.append("counters (mean per dispatch)")
         for (k, c), (v, n) in sorted(cm.items()):
             lines.append(f"{c:>28} {v:>18.1f}  dispatches={n}  {_short(k)}")
+        cv = counter_values(d)
+        busy = {k: v for (k, c), v in cv.items() if c == "SQ_VALU_MFMA_BUSY_CYCLES"}
+        gui = {k: v for (k, c), v in cv.items() if c == "GRBM_GUI_ACTIVE"}
+        both = sorted(k for k in busy if k in gui and len(busy[k]) == len(gui[k]))
+        if both:
+            lines.append(f"MFMA busy per dispatch: SQ_VALU_MFMA_BUSY_CYCLES / ({MI355X_SIMDS} SIMDs x "
+                         f"GRBM_GUI_ACTIVE / {MI355X_XCDS} XCDs)")
+            for k in both:
+                fr = [b / (MI355X_SIMDS * g / MI355X_XCDS) for b, g in zip(busy[k], gui[k]) if g > 0]
+                if any(f > 0 for f in fr):
+                    lines.append("  " + " ".join(f"{f:.3f}" for f in fr) + f"  {_short(k)}")
     return "\n".join(lines)
 
 
