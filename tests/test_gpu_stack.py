@@ -500,7 +500,7 @@ def test_tiny_prefix_cache_trajectory():
     assert rel_inf(host(S.restore_order(b, perm)), base[-1]["x"]) <= TOL["f32"]
 
 
-@pytest.mark.parametrize("kv_parts,extra", [(None, 0), ("4", 0), (None, 64)])
+@pytest.mark.parametrize("kv_parts,extra", [(None, 0), ("4", 0), (None, 64), ("4", 64)])
 def test_prefix_cache_equals_full_cache_bitwise(kv_parts, extra, monkeypatch):
     """At the Wan-1.3B shape (3 layers, RoPE, HSA-75A groups with a 25%
     baseline group reordered to the end) the prefix-only cache changes only
