@@ -230,6 +230,16 @@ ATTN_CASES = [
     ("bf16", 64, 128, 2, 128),
     ("bf16", 4109, 4096, 32, 128),   # two 32-query sub-tiles per wave
     ("bf16", 2000, 2048, 64, 64),    # idem, head_dim 64
+    # key counts around the 96-row key tile and the 3-tile loop unroll: one block, one tile,
+    # one tile + 1 row, two blocks of a second tile, three tiles, three tiles + 1 row, a
+    # ragged 31-row last block
+    ("bf16", 32, 7, 1, 128),
+    ("bf16", 96, 40, 1, 128),
+    ("bf16", 97, 40, 1, 64),
+    ("bf16", 160, 9, 1, 128),
+    ("bf16", 288, 70, 2, 128),
+    ("bf16", 289, 70, 2, 64),
+    ("bf16", 319, 33, 1, 128),
     ("f32", 1024, 342, 4, 64),
     ("f32", 100, 17, 2, 128),
     ("f32", 1, 3, 1, 64),
