@@ -153,8 +153,8 @@ __device__ __forceinline__ RowGemmOut row_gemm_out(const RowGemm& g, int z) {
 hipError_t launch_row_gemm_f32(const RowGemm& g, hipStream_t s);
 
 // Keys/values: rows n < n_split come from (k, v), rows n_split .. n_kv-1 from
-// (k2, v2) at row n - n_split (a cache prefix followed by fresh rows). The
-// bf16 kernel needs n_split to be a multiple of 64 (its key tile).
+// (k2, v2) at row n - n_split (a cache prefix followed by fresh rows); any
+// n_split.
 // bf16 attention. With a workspace of at least attention_parts_bytes(p, ...)
 // bytes the launch may split the cached rows into p <= kMaxKvParts parts
 // (when that fills the CUs better) and merge them in a second kernel.
