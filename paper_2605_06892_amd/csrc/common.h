@@ -114,6 +114,9 @@ struct RowGemm {
   const int32_t* rope_tok;
   const int32_t* rope_pos;
   int rope_outs, rope_dh, rope_nt, rope_nh, rope_f, rope_h, rope_w;
+  // set by the bf16 launcher: workgroups from this index on take halves of
+  // the remaining 256x256 tiles (see gemm_bf16.hip)
+  int split_from;
 };
 
 // Grid coordinates of row m's token for the rotary embedding of g.

@@ -83,20 +83,16 @@ struct Tiling {
   static __device__ __forceinline__ int swz(int r) { return (r / (16 / CHUNKS)) % CHUNKS; }
 };
 
-// NOUT (1 or 3) is the number of outputs sharing A; it is a template
-// parameter so the Q/K/V projection and the output projection are distinct
-// kernels in profiles.
-template <class TL, int NOUT, int EPI>
-__global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
+// Output tile (tm, tn) of output z in tiling TL, staged through the
+// workgroup's LDS arrays L0..L3 (at least TL::STAGE elements each, as many as
+// TL has stages). Each stage is its own array, so that the compiler can tell
+// the asynchronous loads into one stage from the fragment reads of another.
+template <class TL, int EPI, class LA, class LB, class LC, class LD>
+__device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, int z, LA& L0, LB& L1,
+                                              LC& L2, LD& L3) {
   constexpr int BM = TL::BM, BN = TL::BN, BK = TL::BK, STAGES = TL::STAGES, WN = TL::WN;
   constexpr int TM = TL::TM, TN = TL::TN, MI = TL::MI, NI = TL::NI, LOADS = TL::LOADS;
   constexpr int SEG_A = TL::SEG_A, CHUNKS = TL::CHUNKS, SEG_ROWS = TL::SEG_ROWS;
-  // one array per stage, so that the compiler can tell the asynchronous
-  // loads into one stage from the fragment reads of another
-  __shared__ __attribute__((aligned(16))) bf16 L0[TL::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 L1[TL::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 L2[STAGES > 2 ? TL::STAGE : 1];
-  __shared__ __attribute__((aligned(16))) bf16 L3[STAGES > 3 ? TL::STAGE : 1];
   auto stage = [&](auto s) -> bf16* {
     if constexpr (decltype(s)::value == 0) return L0;
     else if constexpr (decltype(s)::value == 1) return L1;
@@ -104,21 +100,6 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
     else return L3;
   };
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
-
-  const int tiles_m = (g.M + BM - 1) / BM;
-  const int tiles_n1 = (g.Nc + BN - 1) / BN;  // per output
-  const int tiles_n = tiles_n1 * NOUT;        // over all outputs side by side
-  const int total = tiles_m * tiles_n;
-  const int item = xcd_contiguous(blockIdx.x, total);
-  // grouped order: kGroupM tile-rows sweep all tile-columns together
-  const int group = item / (kGroupM * tiles_n);
-  const int first_m = group * kGroupM;
-  const int gm = min(kGroupM, tiles_m - first_m);
-  const int r = item - group * kGroupM * tiles_n;
-  const int tm = first_m + r % gm;
-  const int tnc = r / gm;
-  const int z = tnc / tiles_n1;
-  const int tn = tnc - z * tiles_n1;
   const RowGemmOut oz = row_gemm_out(g, z);
 
   const bf16* __restrict__ A = static_cast<const bf16*>(g.A);
@@ -376,10 +357,88 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   }
 }
 
+// The three tilings of 8 waves (see launch_best); a 256 x 256 tile splits
+// into two 256 x 128 halves.
+using TBig = Tiling<256, 256, 64, 2, 8, 2>;
+using T192 = Tiling<256, 192, 64, 2, 8, 4>;
+using TMid = Tiling<256, 128, 64, 2, 8, 4>;
+
+// NOUT (1 or 3) is the number of outputs sharing A; it is a template
+// parameter so the Q/K/V projection and the output projection are distinct
+// kernels in profiles. Workgroup b takes tile item xcd_contiguous(b, tiles):
+// tiles are ordered in groups of kGroupM tile-rows that sweep all tile-columns
+// (of all outputs) together, and each XCD runs a contiguous range of items.
+// With the 256 x 256 tiling, the workgroups from g.split_from on take halves:
+// workgroups split_from + 2j and split_from + 2j + 1 compute the two 256 x 128
+// halves of the tile workgroup split_from + j would have taken. The launcher
+// sets split_from so that a last, partly filled round of big tiles becomes
+// one round of halves.
 template <class TL, int NOUT, int EPI>
-hipError_t launch(const RowGemm& g, hipStream_t s) {
-  const long tiles = (long)((g.M + TL::BM - 1) / TL::BM) * ((g.Nc + TL::BN - 1) / TL::BN) * NOUT;
-  hipLaunchKernelGGL((row_gemm_bf16_kernel<TL, NOUT, EPI>), dim3((unsigned)tiles), dim3(TL::THREADS), 0, s, g);
+__global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
+  constexpr int STAGES = TL::STAGES;
+  constexpr bool kSplit = std::is_same<TL, TBig>::value;
+  static_assert(!kSplit || (TMid::STAGE <= TL::STAGE && TMid::THREADS == TL::THREADS), "halves");
+  __shared__ __attribute__((aligned(16))) bf16 L0[TL::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 L1[TL::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 L2[STAGES > 2 ? TL::STAGE : 1];
+  __shared__ __attribute__((aligned(16))) bf16 L3[STAGES > 3 ? TL::STAGE : 1];
+
+  const int tiles_m = (g.M + TL::BM - 1) / TL::BM;
+  const int tiles_n1 = (g.Nc + TL::BN - 1) / TL::BN;  // per output
+  const int tiles_n = tiles_n1 * NOUT;                 // over all outputs side by side
+  const int total = tiles_m * tiles_n;
+  int b = blockIdx.x, half = -1;
+  if constexpr (kSplit) {
+    if (b >= g.split_from) {
+      half = (b - g.split_from) & 1;
+      b = g.split_from + (b - g.split_from) / 2;
+    }
+  }
+  const int item = xcd_contiguous(b, total);
+  const int group = item / (kGroupM * tiles_n);
+  const int first_m = group * kGroupM;
+  const int gm = min(kGroupM, tiles_m - first_m);
+  const int r = item - group * kGroupM * tiles_n;
+  const int tm = first_m + r % gm;
+  const int tnc = r / gm;
+  const int z = tnc / tiles_n1;
+  const int tn = tnc - z * tiles_n1;
+  if constexpr (kSplit) {
+    if (half >= 0) {
+      row_gemm_tile<TMid, EPI>(g, tm, tn * 2 + half, z, L0, L1, L2, L3);
+      return;
+    }
+  }
+  row_gemm_tile<TL, EPI>(g, tm, tn, z, L0, L1, L2, L3);
+}
+
+// Rounds of a launch of `tiles` tiles on the CUs, in units of a full round
+// of this tiling: with the 256 x 256 tiling, a last round at most half full
+// is run as halves and costs a round of 256 x 128 tiles (kHalfRound).
+constexpr double kHalfRound = 0.675;
+template <class TL>
+bool split_tail(long tiles) {
+  const long cus = compute_units(), rem = tiles % cus;
+  return std::is_same<TL, TBig>::value && tiles > cus && rem > 0 && 2 * rem <= cus;
+}
+template <class TL>
+double rounds(long tiles) {
+  const long cus = compute_units();
+  return split_tail<TL>(tiles) ? (double)(tiles / cus) + kHalfRound : (double)((tiles + cus - 1) / cus);
+}
+
+template <class TL, int NOUT, int EPI>
+hipError_t launch(const RowGemm& g0, hipStream_t s) {
+  const long tiles = (long)((g0.M + TL::BM - 1) / TL::BM) * ((g0.Nc + TL::BN - 1) / TL::BN) * NOUT;
+  RowGemm g = g0;
+  g.split_from = 0x7fffffff;
+  long grid = tiles;
+  if (split_tail<TL>(tiles)) {
+    const long rem = tiles % compute_units();
+    g.split_from = (int)(tiles - rem);
+    grid = tiles + rem;
+  }
+  hipLaunchKernelGGL((row_gemm_bf16_kernel<TL, NOUT, EPI>), dim3((unsigned)grid), dim3(TL::THREADS), 0, s, g);
   return hipGetLastError();
 }
 
@@ -391,21 +450,16 @@ hipError_t launch(const RowGemm& g, hipStream_t s) {
 // rounds = ceil(tiles / CUs) and the per-round cost relative to 256 x 256
 // (tile area x cost per FLOP): 1, 0.855, 0.675. A tiling other than 256 x 256
 // must win by 3%. The narrow fp32 velocity head always takes 256 x 128.
-using TBig = Tiling<256, 256, 64, 2, 8, 2>;
-using T192 = Tiling<256, 192, 64, 2, 8, 4>;
-using TMid = Tiling<256, 128, 64, 2, 8, 4>;
-
 template <class TL>
 double estimate(const RowGemm& g, double per_round) {
   const long tiles = (long)((g.M + TL::BM - 1) / TL::BM) * ((g.Nc + TL::BN - 1) / TL::BN) * g.n_out;
-  const long cus = compute_units();
-  return (double)((tiles + cus - 1) / cus) * per_round;
+  return rounds<TL>(tiles) * per_round;
 }
 
 template <int NOUT, int EPI>
 hipError_t launch_best(const RowGemm& g, hipStream_t s) {
   const double eb = estimate<TBig>(g, 1.0), e192 = estimate<T192>(g, 0.855),
-               em = estimate<TMid>(g, 0.675);
+               em = estimate<TMid>(g, kHalfRound);
   if (e192 < 0.97 * eb && e192 <= em) return launch<T192, NOUT, EPI>(g, s);
   if (em < 0.97 * eb && em < e192) return launch<TMid, NOUT, EPI>(g, s);
   return launch<TBig, NOUT, EPI>(g, s);

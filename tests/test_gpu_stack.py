@@ -115,14 +115,18 @@ def test_linear(dtype, n, d_in, d_out, mode):
 @pytest.mark.parametrize("n,d_in,d_out,mode", [
     (4059, 192, 8256, "plain"),     # 256 x 192 tiles (16 x 43): 3 K steps (odd), ragged rows and columns
     (4059, 448, 8256, "residual"),  # 7 K steps
-    (2049, 320, 16384, "gelu"),     # 256 x 256 tiles (9 x 64): 5 K steps
+    (2049, 320, 16384, "gelu"),     # 256 x 256 tiles (9 x 64 = 576): 5 K steps; the last 64 tiles
+                                    # (the 9th tile-row) run as 256 x 128 halves
+    (2049, 320, 16320, "residual"), # idem, the last column tile 192 wide: its second half is ragged
+    (2049, 320, 16256, "plain"),    # idem, 128 wide: its second half lies past the columns
     (700, 64, 768, "plain"),        # 256 x 128 tiles (a grid of few tiles): 1 K step (no steady-state loop)
     (700, 192, 768, "residual"),    # 3 K steps: one steady-state round then the tail
     (513, 640, 1000, "gelu"),       # 10 K steps, ragged columns
 ])
 def test_linear_k_steps(n, d_in, d_out, mode):
     """The bf16 product over K step counts that exercise the steady-state
-    loop (loads interleaved with the MFMAs) and its tail, on both tilings."""
+    loop (loads interleaved with the MFMAs) and its tail, on all three
+    tilings, and a last round of 256 x 256 tiles run as 256 x 128 halves."""
     rng = np.random.default_rng(n * 7 + d_in)
     x = synth.to_bf16_values(rng.standard_normal((n, d_in)).astype(np.float32))
     w = synth.to_bf16_values((rng.standard_normal((d_out, d_in)) / np.sqrt(d_in)).astype(np.float32))
