@@ -447,9 +447,10 @@ hipError_t launch(const RowGemm& g0, hipStream_t s) {
 // (waves of 64 x 64) about 1.35x (measured on the stack shapes), but their
 // finer grids can fill the last round of a launch better. Each launch takes
 // the tiling with the least estimated time, rounds x cost per round, with
-// rounds = ceil(tiles / CUs) and the per-round cost relative to 256 x 256
-// (tile area x cost per FLOP): 1, 0.855, 0.675. A tiling other than 256 x 256
-// must win by 3%. The narrow fp32 velocity head always takes 256 x 128.
+// rounds as counted by rounds() (ceil(tiles / CUs), or the split tail of
+// 256 x 256) and the per-round cost relative to 256 x 256 (tile area x cost
+// per FLOP): 1, 0.855, 0.675. A tiling other than 256 x 256 must win by 3%.
+// The narrow fp32 velocity head always takes 256 x 128.
 template <class TL>
 double estimate(const RowGemm& g, double per_round) {
   const long tiles = (long)((g.M + TL::BM - 1) / TL::BM) * ((g.Nc + TL::BN - 1) / TL::BN) * g.n_out;
