@@ -308,6 +308,23 @@ __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, 
       row_off[l32] = obase;
       row_buf[l32] = buf;
     }
+    // The residual may be the output itself (h += ...), so the compiler
+    // cannot move a pass's residual load above the previous pass's store: all
+    // of the block's residual loads are issued here, before the staging
+    // writes, whose work then covers their latency.
+    bf16x4 res[QPR / 2];
+    if constexpr (EPI == kEpiBf16Residual) {
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // the row table is visible
+#pragma unroll
+      for (int t = 0; t < QPR / 2; ++t) {
+        const int f = lane + 64 * t;
+        const int r = f / QPR, cq = f - r * QPR;
+        const int n = col0 + cq * 4;
+        res[t] = (bf16x4){};
+        if (row_buf[r] >= 0 && n < g.Nc)
+          res[t] = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + row_off[r] + n);
+      }
+    }
     const float rs = (g.row_scale && m < g.M) ? g.row_scale[m] : 1.f;
     RopeRow rr{0, 0, 0};
     if (rope && buf >= 0) rr = rope_row(g, m);
@@ -347,9 +364,7 @@ __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, 
       if constexpr (EPI == kEpiF32) {
         *reinterpret_cast<f32x4*>(static_cast<float*>(cbase) + o) = v;
       } else {
-        if constexpr (EPI == kEpiBf16Residual)
-          v += __builtin_convertvector(*reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + o),
-                                       f32x4);
+        if constexpr (EPI == kEpiBf16Residual) v += __builtin_convertvector(res[t], f32x4);
         *reinterpret_cast<bf16x4*>(static_cast<bf16*>(cbase) + o) = to_bf16x4(v);
       }
     }
