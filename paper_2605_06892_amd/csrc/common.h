@@ -117,6 +117,7 @@ struct RowGemm {
   // set by the bf16 launcher: workgroups from this index on take halves of
   // the remaining 256x256 tiles (see gemm_bf16.hip)
   int split_from;
+  int group_m;  // set by the bf16 launcher: tile-rows per group of the tile order
 };
 
 // Grid coordinates of row m's token for the rotary embedding of g.
