@@ -64,6 +64,8 @@ def parse():
                    help="skip the Euler and gather bandwidth-stress shapes")
     p.add_argument("--no-extra-timings", action="store_true",
                    help="skip the 100%%-active, cold-cache and other-layout timings of the step")
+    p.add_argument("--no-other-workloads", action="store_true",
+                   help="skip the 720p-shaped block (N = 75600) and the Wan-1.3B-shaped block at 50%%")
     p.add_argument("--no-end-to-end", action="store_true",
                    help="skip the 30-layer sampling loops (HSA vs dense, T = 40)")
     p.add_argument("--end-to-end-only", action="store_true", help="run only the 30-layer sampling loops")
@@ -150,6 +152,42 @@ def time_iteration(b, eul, wl, it, sigmas, steps, warmup, flush=None):
            for k, nm in enumerate(KERNEL_NAMES)}
     layer = [evs[s][1].elapsed_time(evs[s][4]) for s in range(steps)]
     return n, wall, per, layer
+
+
+def workload_item(dev, name, it, steps, warmup=2):
+    """One whole HSA iteration of another single-block workload (its own
+    buffers, KV cache filled by a dense iteration 0): active set with its
+    read-back, Q/K/V + cache overwrite, attention, output projection +
+    scatter and the cached Euler update of N x 16 fp32 latents. Per-call event
+    times, the layer step, the iteration and the attention rate."""
+    import torch
+
+    import synth
+
+    wl = synth.WORKLOADS[name]
+    sig = synth.linear_sigmas(wl.T)
+    _, _, b, eul = setup(wl, "scattered", dev)
+    n, wall, per, layer = time_iteration(b, eul, wl, it, sig, steps, warmup)
+    layer_ms = per["qkv_scatter"] + per["attention"] + per["out_scatter"]
+    res = {
+        "workload": f"{wl.name} single block: N={wl.N} ({'x'.join(map(str, wl.grid))} latent tokens), d={wl.d} "
+                    f"({wl.heads}x{wl.dh} heads), T={wl.T}, budgets {{{','.join(str(g[0]) for g in wl.groups)}}} "
+                    f"by velocity-norm rank, iteration {it}",
+        "n_active": n,
+        "active_fraction": round(n / wl.N, 4),
+        "layer_step_ms": round(layer_ms, 4),
+        "layer_step_ms_dist": dist(layer),
+        "iteration_ms": round(sum(per.values()), 4),
+        "ms_per_step": round(wall, 4),
+        "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "active_attention_tflops": round(attention_flops(n, wl.N, wl.d) / (per["attention"] * 1e-3) / 1e12, 2),
+        "qkv_out_gemm_tflops": round(gemm_flops(n, wl.d) / ((per["qkv_scatter"] + per["out_scatter"]) * 1e-3) / 1e12, 2),
+        "euler_state": f"{wl.N}x{EULER_CHANNELS} fp32",
+        "euler_gbs": round(euler_bytes(wl.N, EULER_CHANNELS, n) / (per["cached_euler"] * 1e-3) / 1e9, 1),
+    }
+    del b, eul
+    torch.cuda.empty_cache()
+    return res
 
 
 def dist(xs):
@@ -301,7 +339,7 @@ def schedule_runtimes(dev, name="wan1.3b"):
     import torch
 
     import synth
-    from paper_2605_06892_amd import layer as L
+    from paper_2605_06892_amd import hsa_step as H
 
     wl = synth.WORKLOADS[name]
     blk, _, b, eul = setup(wl, "scattered", dev)
@@ -325,7 +363,7 @@ def schedule_runtimes(dev, name="wan1.3b"):
     for pname, pre in synth.PRESETS.items():
         layout = "random" if pre["strategy"] == "R" else "scattered"
         budget = synth.assign_budgets(blk["v_group"], pre["groups"], layout)
-        m = L.window_margin(pre["window"], T)
+        m = H.hsa_window_margin(pre["window"], T)
         ms, frac = trajectory(budget, m)
         out[pname] = {"ms": round(ms, 2), "runtime_vs_fm": round(ms / fm_ms, 4),
                       "token_step_fraction": round(frac, 4), "paper_runtime": pre["printed_runtime"]}
@@ -337,10 +375,18 @@ def schedule_runtimes(dev, name="wan1.3b"):
     return out
 
 
+def euler_bytes(n_tokens, channels, n_fresh):
+    """Bytes the one-pass cached Euler update must move: x read and written and
+    one velocity row read per token (cached or fresh), the fresh rows written
+    to the velocity cache, and the index list."""
+    return n_tokens * channels * 4 * 3 + n_fresh * (channels * 4 + 4)
+
+
 def euler_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
     """The cached Euler update at a bandwidth-stress shape (16M tokens x 16 fp32
     channels, every 4th token fresh), far above the 256 MB last-level cache:
-    HBM bytes moved per launch over its event time, against the HBM peak."""
+    algorithmic bytes per launch (euler_bytes) over its event time, against
+    the HBM peak."""
     import torch
 
     from paper_2605_06892_amd import hsa_step as H
@@ -360,7 +406,7 @@ def euler_stress(dev, n_tokens=1 << 24, channels=EULER_CHANNELS, reps=10):
         if r >= 2:
             ts.append(a.elapsed_time(b))
     ms = float(np.median(ts))
-    nbytes = n_tokens * channels * 4 * 3 + na * (channels * 4 * 2 + 4)
+    nbytes = euler_bytes(n_tokens, channels, na)
     gbs = nbytes / (ms * 1e-3) / 1e9
     del x, vc, vf, idx
     return {"tokens": n_tokens, "channels": channels, "fresh_rows": na, "ms": round(ms, 4),
@@ -424,7 +470,6 @@ def end_to_end(dev, name="wan1.3b_stack", presets=False, rope=False):
 
     import synth
     from paper_2605_06892_amd import hsa_step as H
-    from paper_2605_06892_amd import layer as LY
     from paper_2605_06892_amd import stack as S
 
     wl = synth.WORKLOADS[name]
@@ -503,7 +548,7 @@ def end_to_end(dev, name="wan1.3b_stack", presets=False, rope=False):
     if presets:
         for pname, pre in synth.PRESETS.items():
             psizes = synth.group_sizes(N, pre["groups"])
-            m = LY.window_margin(pre["window"], T)
+            m = H.hsa_window_margin(pre["window"], T)
             if pre["strategy"] == "D":
                 ms, r = loop(psizes, margin=m, selection=H.SELECT_L1_REL)
                 how = f"strategy D (L1_rel over iterations 0-{m - 1})"
@@ -524,7 +569,7 @@ def end_to_end(dev, name="wan1.3b_stack", presets=False, rope=False):
         pre = synth.PRESETS["HSA-75A"]
         budget0 = synth.assign_budgets(np.zeros((N, 1), np.float32), pre["groups"], "first_frame",
                                        frame_tokens=wl.grid[1] * wl.grid[2], seed=0)
-        m = LY.window_margin(pre["window"], T)
+        m = H.hsa_window_margin(pre["window"], T)
         n_cached = S.prefix_rows(int(np.sum(budget0 < T)), N)
         pb = S.StackBuffers.allocate(N, C, L, wl.heads, wl.dh, torch.bfloat16, device=dev, ffn=wl.ffn,
                                      ctx=wl.ctx, n_cached=n_cached)
@@ -549,9 +594,10 @@ def end_to_end(dev, name="wan1.3b_stack", presets=False, rope=False):
 
 
 def cpu_baseline(wl, blk, budget, it):
-    """The oracle's layer step timed on this host: two bounded samples of the
-    active rows (projections, attention against the whole N-row cache, output
-    projection and scatter), extrapolated linearly to all active rows."""
+    """The oracle's layer step timed on this host over every active row: the
+    fresh Q/K/V rows and the cache overwrite, attention of all active queries
+    against the whole N-row cache, the output projection and the scatter
+    (oracle.layer_step, float64, queries in blocks of at most 512 rows)."""
     import oracle
     import synth
 
@@ -564,22 +610,13 @@ def cpu_baseline(wl, blk, budget, it):
     k0, v0 = synth.draw_cache(wl.N, wl.d, seed=1, dtype="bf16")
     out0 = np.zeros((wl.N, wl.d), np.float32)
     w = {k: blk[k] for k in ("wq", "wk", "wv", "wo")}
-    rng = np.random.default_rng(0)
-    times = {}
-    lo, hi = 512, 2048  # about 10 s of oracle work on 16 host threads
-    for s in (lo, hi):
-        sub = np.sort(rng.choice(idx, size=min(s, idx.size), replace=False))
-        t0 = time.perf_counter()
-        oracle.layer_step(blk["x"], sub, w, k0, v0, out0, wl.heads, wl.dh, 1 / math.sqrt(wl.dh), "bf16")
-        times[s] = time.perf_counter() - t0
-    per_row = max((times[hi] - times[lo]) / (hi - lo), 0.0)
-    fixed = max(times[lo] - lo * per_row, 0.0)
-    est_ms = (fixed + per_row * idx.size) * 1e3
-    return {"value": round(est_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+    t0 = time.perf_counter()
+    oracle.layer_step(blk["x"], idx, w, k0, v0, out0, wl.heads, wl.dh, 1 / math.sqrt(wl.dh), "bf16")
+    ms = (time.perf_counter() - t0) * 1e3
+    return {"value": round(ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
             "host_cpus": os.cpu_count(),
-            "sample": (f"oracle.layer_step on {lo} and {hi} of the {idx.size} active rows (all {wl.N} cached rows, "
-                       f"{wl.heads} heads), {times[lo]:.1f}s + {times[hi]:.1f}s; linear fit extrapolated to "
-                       f"all {idx.size} active rows")}
+            "sample": (f"full step, {idx.size} rows: one oracle.layer_step over all {idx.size} active rows "
+                       f"(iteration {it}) against all {wl.N} cached rows, {wl.heads} heads, float64, timed once")}
 
 
 def main():
@@ -614,7 +651,9 @@ def main():
         print(json.dumps(out))
         return
     if args.only == "stress":
-        print(json.dumps({"gather_stress": gather_stress(dev), "euler_stress": euler_stress(dev)}))
+        print(json.dumps({"gather_stress": gather_stress(dev), "euler_stress": euler_stress(dev),
+                          "euler_stress_c64": euler_stress(dev, n_tokens=1 << 22, channels=64),
+                          "gather_stress_c64": gather_stress(dev, n_tokens=1 << 22, channels=64)}))
         return
     wl = synth.WORKLOADS[args.workload]
     sigmas = synth.linear_sigmas(wl.T)
@@ -650,7 +689,7 @@ def main():
     attn_fl = attention_flops(n, wl.N, wl.d)
     attn_tflops = attn_fl / (per["attention"] * 1e-3) / 1e12
     gemm_tf = gemm_flops(n, wl.d) / ((per["qkv_scatter"] + per["out_scatter"]) * 1e-3) / 1e12
-    euler_bytes = (wl.N * EULER_CHANNELS * 4 * 3) + n * EULER_CHANNELS * 4 * 2 + n * 4
+    eb = euler_bytes(wl.N, EULER_CHANNELS, n)
     out = {
         "metric": METRIC,
         "value": round(layer_ms, 4),
@@ -677,7 +716,7 @@ def main():
         "layer_step_ms_dist": dist(layer),
         "active_attention_tflops": round(attn_tflops, 2),
         "qkv_out_gemm_tflops": round(gemm_tf, 2),
-        "euler_gbs": round(euler_bytes / (per["cached_euler"] * 1e-3) / 1e9, 1),
+        "euler_gbs": round(eb / (per["cached_euler"] * 1e-3) / 1e9, 1),
     }
     out["roofline"] = {
         "kernel": "attention_bf16",
@@ -720,10 +759,18 @@ def main():
         b.budget.copy_(torch.from_numpy(budget))
     if not args.no_euler_stress:
         out["euler_stress"] = euler_stress(dev)
+        # 64 fp32 channels: the stack's latent rows, 256 bytes, whole cache lines
+        out["euler_stress_c64"] = euler_stress(dev, n_tokens=1 << 22, channels=64)
         out["gather_stress"] = gather_stress(dev)
-    if not args.no_schedules or not args.no_end_to_end:
+        # the stack's real latent rows: 64 fp32 channels (256-byte rows, whole cache lines)
+        out["gather_stress_c64"] = gather_stress(dev, n_tokens=1 << 22, channels=64)
+    if not args.no_schedules or not args.no_end_to_end or not args.no_other_workloads:
         del b, eul
         torch.cuda.empty_cache()
+    if not args.no_other_workloads:
+        # the 720p-shaped block (N = 75600, 25% active) and the Wan-1.3B-shaped block at 50%
+        out["wan14b_720p"] = workload_item(dev, "wan14b_720p", 1, max(5, args.steps // 4))
+        out["wan13b_50"] = workload_item(dev, "wan1.3b", 2, args.steps)
     if not args.no_schedules:
         out["schedules"] = schedule_runtimes(dev)
         torch.cuda.empty_cache()

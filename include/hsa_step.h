@@ -101,6 +101,19 @@ int hsa_build_active_set(const int32_t* budget, int64_t n_tokens, int32_t T, int
                          int32_t* n_active_host, hipStream_t stream);
 
 /*
+ * Margin m of a phase-aware caching window over the centre k% of a T-step
+ * trajectory (Section 2.5: m = floor((1 - k) T / 2)), in exact integer
+ * arithmetic: m = ((100 - center_percent) * T) div 200. (Evaluated in
+ * floating point, (1 - 0.8) * 40 / 2 falls just below 4 and floors to 3;
+ * the printed HSA-50 runtime of Appendix C, 50%, needs m = 4: 49.6% of the
+ * token-steps, against 47.5% with m = 3.) Host-only; enqueues nothing.
+ *   center_percent   0 <= k <= 100 (100: no window, m = 0)
+ *   T                T >= 1
+ * Returns m (0 <= m <= T/2), or -1 for arguments out of range.
+ */
+int32_t hsa_window_margin(int32_t center_percent, int32_t T);
+
+/*
  * The same with a choice of what happens outside the window (Section 2.5
  * says every token is active there; read literally, the HSA-25 preset of
  * Appendix C then takes 34.8% of the token-steps instead of its printed 25%).
@@ -217,7 +230,12 @@ int hsa_active_attention(int dtype, const void* q, const void* k_cache, const vo
  *                       (active tokens take their fresh velocity);
  *   then x[n, c] = fmaf(v_cache[n, c], sigma_next - sigma_i, x[n, c]) for every
  *   n < n_tokens, c < channels, the difference taken in fp32.
+ * One pass over the tokens (one kernel): every token reads its fresh row or
+ * its cached row, x is advanced, and only fresh rows are written to v_cache.
  *   x, v_cache      [n_tokens, channels] fp32; v_fresh [n_active, channels].
+ *   idx             int32 [n_active], strictly ascending, in [0, n_tokens)
+ *                   (as hsa_build_active_set produces it). For another order
+ *                   the result is unspecified (no access outside the buffers).
  * With v_fresh == NULL, idx and n_active are ignored (the velocity cache is
  * already current, e.g. it was the scatter target of hsa_out_scatter).
  * x must not overlap v_cache or v_fresh; v_fresh must not overlap v_cache.
@@ -456,11 +474,14 @@ typedef struct hsa_stack {
  *      HSA_SELECT_VELOCITY_NORM: if i is a multiple of P = lcm over the group
  *        budgets of T / s_k (the iterations where every group's schedule
  *        fires), the budgets are reassigned from v_hat as hsa_assign_budgets.
- *        A refresh iteration where not every token is active returns
- *        HSA_STEP_ERR_BUDGET after step 3 (the budgets in force did not come
- *        from the group table).
+ *        A refresh iteration where not every token is active (the budgets in
+ *        force did not come from the group table) returns HSA_STEP_ERR_BUDGET
+ *        right after step 1: x, v_hat, the budgets and the caches are left
+ *        unchanged (only the idx and n_active scratch are written).
  *      HSA_SELECT_L1_REL (strategy D; needs margin >= 2 and outside_period
- *        1): at iterations i < margin (every token active) the fresh
+ *        1; an iteration i < margin where not every token is active returns
+ *        HSA_STEP_ERR_BUDGET right after step 1, as above): at iterations
+ *        i < margin (every token active) the fresh
  *        velocities feed hsa_l1_rel_accumulate into the keys scratch (first
  *        at i = 0; the keys buffer carries the sums from one call to the
  *        next), and at i = margin - 1 the budgets are assigned from the sums

@@ -21,6 +21,11 @@ HSA_API const char* hsa_step_status_string(int status) {
   }
 }
 
+HSA_API int32_t hsa_window_margin(int32_t center_percent, int32_t T) {
+  if (center_percent < 0 || center_percent > 100 || T < 1) return -1;
+  return (int32_t)(((int64_t)(100 - center_percent) * T) / 200);
+}
+
 HSA_API int hsa_build_active_set_window(const int32_t* budget, int64_t n_tokens, int32_t T,
                                         int32_t iter, int32_t margin, int32_t outside_period,
                                         int32_t* idx, int32_t* n_active_dev,

@@ -384,6 +384,11 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   }
   if (n_active_host) *n_active_host = n;
   if (refreshed_host) *refreshed_host = 0;
+  // a refresh iteration (step 4) needs a fresh velocity for every token: refuse
+  // it before anything that changes the caller's state is enqueued
+  const bool refresh_now = n_groups && !l1rel && iter % refresh_period(T, group_budget, n_groups) == 0;
+  const bool l1_now = l1rel && iter < margin;
+  if ((refresh_now || l1_now) && n != N) return HSA_STEP_ERR_BUDGET;
 
   // 2. the stack on the active rows
   const int dt = s->dtype;
@@ -475,14 +480,12 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
 
   // 4. group membership
   double* keys = static_cast<double*>(s->keys);
-  if (n_groups && !l1rel && iter % refresh_period(T, group_budget, n_groups) == 0) {
-    if (n != N) return HSA_STEP_ERR_BUDGET;
+  if (refresh_now) {
     if (!ok(hsa::launch_assign_budgets(s->v_hat, N, C, tab, keys, s->budget, stream)))
       return HSA_STEP_ERR_LAUNCH;
     if (refreshed_host) *refreshed_host = 1;
   }
-  if (l1rel && iter < margin) {
-    if (n != N) return HSA_STEP_ERR_BUDGET;
+  if (l1_now) {
     if (!ok(hsa::launch_l1_rel(s->v_hat, s->v_prev, N, C, keys, iter == 0, stream)))
       return HSA_STEP_ERR_LAUNCH;
     if (iter == margin - 1) {

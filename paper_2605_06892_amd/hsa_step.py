@@ -53,6 +53,7 @@ def lib() -> ctypes.CDLL:
             "hsa_step_status_string": (ctypes.c_char_p, [ctypes.c_int]),
             "hsa_build_active_set": (ctypes.c_int, [P, I64, I32, I32, I32, P, P, P, P]),
             "hsa_build_active_set_window": (ctypes.c_int, [P, I64, I32, I32, I32, I32, P, P, P, P]),
+            "hsa_window_margin": (I32, [I32, I32]),
             "hsa_qkv_scatter": (ctypes.c_int, [ctypes.c_int, P, I32, P, I32, I64, I32, P, P, P, P, P, P, P]),
             "hsa_attention_core": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P]),
             "hsa_attention_core_parts": (ctypes.c_int, [ctypes.c_int, P, P, P, I32, I64, I32, I32, F, P, P, S, P]),
@@ -87,6 +88,7 @@ EXPORTED = (
     "hsa_step_status_string",
     "hsa_build_active_set",
     "hsa_build_active_set_window",
+    "hsa_window_margin",
     "hsa_qkv_scatter",
     "hsa_attention_core",
     "hsa_attention_core_parts",
@@ -169,6 +171,14 @@ def _dev(*ts) -> None:
     for t in ts:
         if t is not None and (not t.is_cuda or not t.is_contiguous()):
             raise ValueError("tensors must be contiguous device tensors")
+
+
+def hsa_window_margin(center_percent: int, T: int) -> int:
+    """Margin of a caching window over the centre center_percent% of T steps."""
+    m = lib().hsa_window_margin(int(center_percent), int(T))
+    if m < 0:
+        raise ValueError(f"hsa_window_margin: arguments out of range ({center_percent}, {T})")
+    return m
 
 
 def hsa_build_active_set(budget, T: int, iteration: int, margin: int, idx, n_active_dev,

@@ -73,14 +73,6 @@ class BlockBuffers:
                    n_active=e(1, dt=torch.int32), heads=heads, head_dim=head_dim, parts=parts)
 
 
-def window_margin(center_percent: int, T: int) -> int:
-    """Margin m of a caching window over the centre k% of a T-step trajectory,
-    m = floor((1 - k) T / 2) (Section 2.5), in exact integer arithmetic."""
-    if not 0 <= center_percent <= 100:
-        raise ValueError("window percent out of range")
-    return ((100 - center_percent) * T) // 200
-
-
 def active_set(b: BlockBuffers, T: int, iteration: int, margin: int = 0, outside_period: int = 1) -> int:
     """A_i into b.idx; returns |A_i| (one stream synchronization)."""
     return H.hsa_build_active_set(b.budget, T, iteration, margin, b.idx, b.n_active,

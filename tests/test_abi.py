@@ -32,7 +32,7 @@ W = 0x7F6000000000
 
 def declared_functions():
     text = open(HEADER).read()
-    return re.findall(r"^(?:int|size_t|const char\*)\s+(hsa_\w+)\s*\(", text, flags=re.M)
+    return re.findall(r"^(?:int|int32_t|size_t|const char\*)\s+(hsa_\w+)\s*\(", text, flags=re.M)
 
 
 @pytest.fixture(scope="module")
@@ -66,6 +66,25 @@ def test_status_strings(lib):
     for s in range(8):
         assert lib.hsa_step_status_string(s)
     assert lib.hsa_step_status_string(99) == b"unknown status"
+
+
+def test_window_margin(lib):
+    # Section 2.5, m = floor((1 - k) T / 2) in exact integers (HSA-50: k = 80%, T = 40 -> 4, not 3)
+    assert lib.hsa_window_margin(80, 40) == 4
+    assert lib.hsa_window_margin(50, 40) == 10
+    assert lib.hsa_window_margin(100, 40) == 0
+    assert lib.hsa_window_margin(0, 40) == 20
+    assert lib.hsa_window_margin(0, 7) == 3
+    for bad in ((-1, 40), (101, 40), (50, 0), (50, -3)):
+        assert lib.hsa_window_margin(*bad) == -1
+    # every margin it returns is one hsa_build_active_set accepts (0 <= m <= T/2)
+    for T in range(1, 81):
+        for k in range(101):
+            m = lib.hsa_window_margin(k, T)
+            assert 0 <= m <= T // 2 and m == ((100 - k) * T) // 200
+    assert H.hsa_window_margin(80, 40) == 4
+    with pytest.raises(ValueError):
+        H.hsa_window_margin(120, 40)
 
 
 def test_workspace_bytes(lib):

@@ -132,6 +132,34 @@ def test_cached_euler(N, C, fresh):
     assert np.mean(host(x) == x_ref) > 0.9999
 
 
+def _euler_patterns(N):
+    rng = np.random.default_rng(N)
+    return {
+        "all": np.arange(N),
+        "first": np.array([0]),
+        "last": np.array([N - 1]),
+        "run": np.arange(N // 3, min(N, N // 3 + 700)),  # crosses token-tile boundaries
+        "every_other": np.arange(1, N, 2),
+        "random": np.sort(rng.choice(N, size=max(1, N // 5), replace=False)),
+    }
+
+
+@pytest.mark.parametrize("N,C", [(3000, 16), (1100, 7), (300, 4096), (200, 4100), (5000, 1)])
+def test_cached_euler_index_patterns(N, C):
+    # one pass over the tokens: fresh rows taken from v_fresh through the ascending
+    # index list, cached rows otherwise; x within one rounding of the oracle
+    s = synth.linear_sigmas(40)
+    for name, idx_np in _euler_patterns(N).items():
+        st = synth.draw_euler_state(N, C, idx_np.size, seed=N * 7 + C)
+        x, vc = to_dev(st["x"], "f32"), to_dev(st["v_cache"], "f32")
+        H.hsa_cached_euler(x, vc, to_dev(st["v_fresh"], "f32"), i32(idx_np), idx_np.size, float(s[3]),
+                           float(s[4]))
+        x_ref, v_ref = oracle.cached_euler(st["x"], st["v_cache"], st["v_fresh"], idx_np, s[3], s[4])
+        np.testing.assert_array_equal(host(vc), v_ref, err_msg=name)
+        assert rel_inf(host(x), x_ref) <= 1e-6, name
+        assert np.mean(host(x) == x_ref) > 0.9999, name
+
+
 def test_cached_euler_fp32_step_difference():
     # the shared step is sigma_next - sigma_i taken in fp32
     x = torch.zeros(4, 4, device=DEV)

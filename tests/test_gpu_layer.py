@@ -7,8 +7,13 @@
 * The Wan-shaped bf16 workloads run one iteration at full size in the launch
   configuration the benchmark times. The oracle computes the fresh K/V rows
   of every active token (the full cache is needed by any query) but only a
-  seeded sample of active query rows through attention and the output
+  seeded sample of 512 active query rows through attention and the output
   projection; skipped cache and output rows are compared bit for bit in full.
+  The Wan-14B block is run at 25%, 50% and 100% active, in the scattered and
+  contiguous budget layouts. At 100% (iteration 8, where every budget's
+  schedule fires) the HSA step is the dense step (Section 2.3): the index list
+  is the identity, every output row is written and finite, and the sampled
+  rows match the oracle's dense step.
 """
 
 import math
@@ -59,8 +64,11 @@ FULL = [
     ("wan14b", 1, "scattered"),
     ("wan14b", 1, "contiguous"),
     ("wan14b", 2, "scattered"),
+    ("wan14b", 2, "contiguous"),
+    ("wan14b", 8, "scattered"),       # every token active: the dense step, 5120 attention workgroups
     ("wan14b_720p", 1, "scattered"),  # N = 75600, 18900 active rows
 ]
+SAMPLED_ROWS = 512
 
 
 @pytest.mark.parametrize("name,it,layout", FULL, ids=lambda v: str(v))
@@ -84,8 +92,16 @@ def test_full_shape_iteration(name, it, layout):
     n = L.active_set(b, wl.T, it)
     assert n == idx_ref.size
     np.testing.assert_array_equal(b.idx[:n].cpu().numpy(), idx_ref)
+    print(f"full-shape iteration {name} i={it} {layout}: |A|={n} of N={N}", flush=True)
     L.layer_step(b, n)
     torch.cuda.synchronize()
+    if n == N:
+        # all active: the identity index list, every output row written (none keeps its old
+        # value) and finite
+        np.testing.assert_array_equal(idx_ref, np.arange(N))
+        assert bool(torch.isfinite(b.out).all()) and bool(torch.isfinite(b.o[:n]).all())
+        changed = (b.out.view(torch.int16) != to_dev(out0, "bf16").view(torch.int16)).any(dim=1)
+        assert int(changed.sum()) == N
 
     # skipped rows: bit for bit untouched
     skipped = np.setdiff1d(np.arange(N), idx_ref)
@@ -106,7 +122,7 @@ def test_full_shape_iteration(name, it, layout):
 
     # sampled active query rows through attention and the output projection
     rng = np.random.default_rng(it)
-    js = np.sort(rng.choice(n, size=min(n, 192), replace=False))
+    js = np.sort(rng.choice(n, size=min(n, SAMPLED_ROWS), replace=False))
     q_s = oracle.project(xa[js], blk["wq"], "bf16")
     assert rel_inf(host(b.q[torch.from_numpy(js).to(DEV)]), q_s) <= 1e-2
     r = oracle.attention_output(q_s, k_full, v_full, blk["wo"], wl.heads, wl.dh, 1 / math.sqrt(wl.dh), "bf16")
