@@ -224,6 +224,36 @@ int hsa_active_attention(int dtype, const void* q, const void* k_cache, const vo
                          int32_t head_dim, float scale, const void* wo, void* out,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Size of the fixed device scratch of hsa_active_attention_noalloc: 96 MiB. */
+#define HSA_STEP_NOALLOC_SCRATCH_BYTES (96u << 20)
+
+/*
+ * hsa_active_attention without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, results and checks as
+ * hsa_active_attention, with the workspace taken from a fixed array of
+ * HSA_STEP_NOALLOC_SCRATCH_BYTES bytes in this library's device code: each
+ * GPU the library runs on holds its own array until the process ends. The
+ * call allocates nothing (no hipMalloc, no allocating library call). Its
+ * first call on a device looks up the array's address there (the device the
+ * stream belongs to must be current).
+ *   Limit: hsa_attention_workspace_bytes(dtype, n_active, heads * head_dim)
+ *   must not exceed HSA_STEP_NOALLOC_SCRATCH_BYTES (bf16 at d = 5120: up to
+ *   9830 active rows; at d = 1536: up to 32768), else HSA_STEP_ERR_WORKSPACE
+ *   and nothing is enqueued. Bytes past the compact output may hold key parts
+ *   as for hsa_active_attention.
+ *   Every call on one GPU shares that GPU's array: calls that may overlap in
+ *   time on one GPU (different streams, different host threads without
+ *   ordering) race and give unspecified results. Calls on one stream are
+ *   ordered and safe. Nothing in the array needs to start at zero.
+ * HSA_STEP_ERR_LAUNCH if the array's address cannot be found on the current
+ * device.
+ */
+int hsa_active_attention_noalloc(int dtype, const void* q, const void* k_cache,
+                                 const void* v_cache, const int32_t* idx, int32_t n_active,
+                                 int64_t n_tokens, int32_t heads, int32_t head_dim, float scale,
+                                 const void* wo, void* out, hipStream_t stream);
+
 /*
  * Cached Euler update (Section 2.4, Eq. 6), fp32, for all n_tokens tokens:
  *   if v_fresh != NULL: v_cache[idx[j]] = v_fresh[j] for j < n_active

@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
             "hsa_attention_workspace_bytes": (S, [ctypes.c_int, I32, I32]),
             "hsa_attention_parts_workspace_bytes": (S, [ctypes.c_int, I32, I32, I32]),
             "hsa_active_attention": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P, S, P]),
+            "hsa_active_attention_noalloc": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I32, I64, I32, I32, F, P, P, P]),
             "hsa_cached_euler": (ctypes.c_int, [P, P, P, P, I32, I64, I32, F, F, P]),
             "hsa_gather_rows": (ctypes.c_int, [ctypes.c_int, P, P, I32, I64, I32, P, P]),
             "hsa_row_rms_scale": (ctypes.c_int, [ctypes.c_int, P, I32, I32, F, P, P]),
@@ -96,6 +97,7 @@ EXPORTED = (
     "hsa_attention_workspace_bytes",
     "hsa_attention_parts_workspace_bytes",
     "hsa_active_attention",
+    "hsa_active_attention_noalloc",
     "hsa_cached_euler",
     "hsa_gather_rows",
     "hsa_row_rms_scale",
@@ -257,6 +259,16 @@ def hsa_active_attention(q, k_cache, v_cache, idx, n_active: int, heads: int, he
                                     k_cache.shape[0], heads, head_dim, scale, _ptr(wo), _ptr(out),
                                     _ptr(workspace), nbytes, _stream(stream))
     _check("hsa_active_attention", st)
+
+
+def hsa_active_attention_noalloc(q, k_cache, v_cache, idx, n_active: int, heads: int, head_dim: int,
+                                 scale: float, wo, out, stream=None) -> None:
+    _dev(q, k_cache, v_cache, idx, wo, out)
+    dt = _dtype(q, k_cache, v_cache, wo, out)
+    st = lib().hsa_active_attention_noalloc(dt, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(idx), n_active,
+                                            k_cache.shape[0], heads, head_dim, scale, _ptr(wo), _ptr(out),
+                                            _stream(stream))
+    _check("hsa_active_attention_noalloc", st)
 
 
 def hsa_cached_euler(x, v_cache, v_fresh, idx, n_active: int, sigma_i: float, sigma_next: float,

@@ -68,6 +68,15 @@ def test_status_strings(lib):
     assert lib.hsa_step_status_string(99) == b"unknown status"
 
 
+def test_noalloc_limit_checked_before_anything(lib):
+    # beyond the fixed array: refused on the host, before any HIP call (fake pointers, no GPU)
+    f = lib.hsa_active_attention_noalloc
+    assert f(BF16, A, B, C, D, 9831, 32760, 40, 128, 0.088, E, G, None) == WORKSPACE
+    assert f(7, A, B, C, D, 10, 100, 2, 64, 0.125, E, G, None) == DTYPE
+    assert f(BF16, A, B, C, D, 10, 5, 2, 64, 0.125, E, G, None) == SHAPE
+    assert f(BF16, A, B, C, D, 0, 5, 2, 64, 0.125, E, G, None) == OK  # nothing to do
+
+
 def test_window_margin(lib):
     # Section 2.5, m = floor((1 - k) T / 2) in exact integers (HSA-50: k = 80%, T = 40 -> 4, not 3)
     assert lib.hsa_window_margin(80, 40) == 4
