@@ -93,7 +93,9 @@ const char* hsa_step_status_string(int status);
  *   n_active_host      optional host int32*: if not NULL the call copies
  *                      n_active_dev to it and synchronizes the stream (the one
  *                      per-iteration host read-back), and returns
- *                      HSA_STEP_ERR_BUDGET if a budget was invalid.
+ *                      HSA_STEP_ERR_BUDGET if a budget was invalid. Pinned
+ *                      host memory (hipHostMalloc) makes the copy a direct
+ *                      DMA; pageable memory works too.
  *   n_tokens           0 <= n_tokens < 2^31.
  */
 int hsa_build_active_set(const int32_t* budget, int64_t n_tokens, int32_t T, int32_t iter,

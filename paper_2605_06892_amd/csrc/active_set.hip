@@ -10,14 +10,22 @@
 // schedule there, the reading under which the HSA-25 preset of Appendix C
 // meets its printed runtime).
 //
-// The budget array is small (4 bytes per token: 131 KB at N = 32760), so one
-// workgroup of 1024 threads walks it in chunks of 16384 tokens: each thread
-// classifies 16 consecutive tokens, a wave prefix sum plus a 16-entry LDS scan
-// gives each thread its output offset, and the thread writes its active token
-// indices in order. The result is ascending by construction. Budget validity
-// and activity per budget value come from a per-launch LDS table (T <= 1024),
-// so the hot loop has no integer division.
+// The budget array is small (4 bytes per token: 131 KB at N = 32760), so the
+// work is latency-bound. Up to 16 workgroups of 1024 threads each take one
+// contiguous range of the tokens. A workgroup first counts the active tokens
+// of all ranges before its own (every workgroup reads that prefix itself:
+// there is no scratch memory to pass counts between workgroups, and the
+// prefix reads hit the L2), then walks its range in chunks of 16384 tokens:
+// each thread classifies 16 consecutive tokens, a wave prefix sum plus a
+// 16-entry LDS scan gives each thread its output offset, and the thread
+// writes its active token indices in order. The result is ascending by
+// construction. Budget validity and activity per budget value come from a
+// per-launch LDS table (T <= 1024), so the hot loop has no integer division.
+// The last workgroup has seen every token (its prefix and its own range), so
+// it alone writes |A_i|, or -1 if any budget is invalid.
 #include "common.h"
+
+#include <algorithm>
 
 namespace hsa {
 namespace {
@@ -34,14 +42,30 @@ __device__ __forceinline__ int classify(int s, int T, int iter, bool outside, bo
   return (iter % (T / s)) == 0 ? 2 : 1;
 }
 
+// Sum of v over the workgroup (every thread gets it). Uses red[], which the
+// caller must not be using; ends with a barrier.
+__device__ __forceinline__ int block_sum(int v, int* red) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  int total = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) total += red[i];
+  __syncthreads();
+  return total;
+}
+
+// Workgroup b takes tokens [b * range, min(n, (b + 1) * range)); range is a
+// multiple of 4.
 __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __restrict__ budget,
-                                                              int n, int T, int iter, int margin,
-                                                              int outside_period,
+                                                              int n, int range, int T, int iter,
+                                                              int margin, int outside_period,
                                                               int32_t* __restrict__ idx,
                                                               int32_t* __restrict__ n_active) {
   __shared__ int wave_total[kThreads / kWave];
   __shared__ unsigned char table[kMaxTableT + 1];
-  __shared__ int bad_any;
 
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
@@ -49,20 +73,48 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
   const bool outside = margin > 0 && (iter < margin || iter > T - margin - 1);
   const bool outside_active = outside && (iter % outside_period) == 0;
   const bool use_table = T <= kMaxTableT;
-  if (t == 0) bad_any = 0;
   if (use_table) {
     for (int s = t; s <= T; s += kThreads)
       table[s] = (unsigned char)classify(s, T, iter, outside, outside_active);
   }
   __syncthreads();
+  auto cls_of = [&](int s) {
+    if (use_table) return (s >= 1 && s <= T) ? (int)table[s] : 0;
+    return classify(s, T, iter, outside, outside_active);
+  };
 
   const bool aligned = (reinterpret_cast<uintptr_t>(budget) & 15) == 0;
-  int base = 0;  // active tokens before the current chunk
+  const int r0 = (int)min((long)blockIdx.x * range, (long)n);
+  const int r1 = (int)min((long)r0 + range, (long)n);
   int bad = 0;
-  for (int c0 = 0; c0 < n; c0 += kChunk) {
+  // active tokens before this workgroup's range
+  int before_me = 0;
+  if (r0 > 0) {
+    int cnt = 0;
+    for (int e = t * 4; e < r0; e += kThreads * 4) {  // r0 is a multiple of 4
+      int b4[4];
+      if (aligned) {
+        const int4 v = *reinterpret_cast<const int4*>(budget + e);
+        b4[0] = v.x; b4[1] = v.y; b4[2] = v.z; b4[3] = v.w;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) b4[r] = budget[e + r];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c = cls_of(b4[r]);
+        bad |= (c == 0);
+        cnt += (c == 2);
+      }
+    }
+    before_me = block_sum(cnt, wave_total);
+  }
+
+  int base = before_me;  // active tokens before the current chunk
+  for (int c0 = r0; c0 < r1; c0 += kChunk) {
     const int e0 = c0 + t * kPer;
     int b[kPer];
-    if (aligned && e0 + kPer <= n) {
+    if (aligned && e0 + kPer <= r1) {
       const int4* p = reinterpret_cast<const int4*>(budget + e0);
 #pragma unroll
       for (int r = 0; r < kPer / 4; ++r) {
@@ -74,16 +126,13 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
       }
     } else {
 #pragma unroll
-      for (int r = 0; r < kPer; ++r) b[r] = (e0 + r < n) ? budget[e0 + r] : 0;
+      for (int r = 0; r < kPer; ++r) b[r] = (e0 + r < r1) ? budget[e0 + r] : 0;
     }
     unsigned mask = 0;
 #pragma unroll
     for (int r = 0; r < kPer; ++r) {
-      if (e0 + r < n) {
-        const int s = b[r];
-        int cls;
-        if (use_table) cls = (s >= 1 && s <= T) ? table[s] : 0;
-        else cls = classify(s, T, iter, outside, outside_active);
+      if (e0 + r < r1) {
+        const int cls = cls_of(b[r]);
         bad |= (cls == 0);
         mask |= (cls == 2 ? 1u : 0u) << r;
       }
@@ -113,17 +162,24 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
     base += total;
     __syncthreads();  // wave_total is rewritten by the next chunk
   }
-  if (bad) atomicOr(&bad_any, 1);
-  __syncthreads();
-  if (t == 0) n_active[0] = bad_any ? -1 : base;
+  if (blockIdx.x == gridDim.x - 1) {  // this workgroup has seen every token
+    const int any_bad = block_sum(bad, wave_total);
+    if (t == 0) n_active[0] = any_bad ? -1 : base;
+  }
 }
 
 }  // namespace
 
 hipError_t launch_active_set(const int32_t* budget, int n, int T, int iter, int margin,
                              int outside_period, int32_t* idx, int32_t* n_active, hipStream_t s) {
-  hipLaunchKernelGGL(active_set_kernel, dim3(1), dim3(kThreads), 0, s, budget, n, T, iter, margin,
-                     outside_period, idx, n_active);
+  // up to 16 ranges of at least 4096 tokens (a multiple of 4 each)
+  constexpr int kMaxGroups = 16, kMinRange = 4096;
+  int groups = (int)std::min<long>(kMaxGroups, std::max<long>(1, ((long)n + kMinRange - 1) / kMinRange));
+  int range = (int)((((long)n + groups - 1) / groups + 3) / 4 * 4);
+  if (range < 4) range = 4;
+  groups = (int)std::max<long>(1, ((long)n + range - 1) / range);
+  hipLaunchKernelGGL(active_set_kernel, dim3(groups), dim3(kThreads), 0, s, budget, n, range, T, iter,
+                     margin, outside_period, idx, n_active);
   return hipGetLastError();
 }
 

@@ -27,4 +27,16 @@ inline int launch_status(hipError_t e) { return e == hipSuccess ? HSA_STEP_OK : 
 
 constexpr int64_t kMaxRows = INT32_MAX;
 
+// Largest tensor the entry points accept, in bytes: far above any device's
+// memory (MI355X: 288 GB < 2^39), and low enough that no size product in the
+// checks can overflow.
+constexpr int64_t kMaxBytes = int64_t(1) << 48;
+
+// True if a * b * c (all non-negative) is at most kMaxBytes; the product is
+// formed in 128 bits, so it cannot wrap.
+inline bool fits(int64_t a, int64_t b, int64_t c = 1) {
+  if (a < 0 || b < 0 || c < 0) return false;
+  return (__int128)a * b * c <= (__int128)kMaxBytes;
+}
+
 }  // namespace hsa_api

@@ -42,12 +42,12 @@ HSA_API int hsa_build_active_set_window(const int32_t* budget, int64_t n_tokens,
                                         n_active_dev, stream);
   if (e != hipSuccess) return HSA_STEP_ERR_LAUNCH;
   if (n_active_host) {
-    int32_t v = 0;
-    if (hipMemcpyAsync(&v, n_active_dev, sizeof(v), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+    // straight into the caller's int: a direct DMA when it is pinned host memory
+    if (hipMemcpyAsync(n_active_host, n_active_dev, sizeof(int32_t), hipMemcpyDeviceToHost, stream) !=
+            hipSuccess ||
         hipStreamSynchronize(stream) != hipSuccess)
       return HSA_STEP_ERR_LAUNCH;
-    *n_active_host = v;
-    if (v < 0) return HSA_STEP_ERR_BUDGET;
+    if (*n_active_host < 0) return HSA_STEP_ERR_BUDGET;
   }
   return HSA_STEP_OK;
 }
@@ -68,6 +68,7 @@ HSA_API int hsa_qkv_scatter(int dtype, const void* x, int32_t x_compact, const i
   if (d <= 0 || n_active < 0 || n_tokens < 0 || n_tokens > kMaxRows || n_active > n_tokens)
     return HSA_STEP_ERR_SHAPE;
   if (dtype == HSA_STEP_BF16 && d % 64 != 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, d, es) || !fits(d, d, es)) return HSA_STEP_ERR_SHAPE;
   if (n_active == 0) return HSA_STEP_OK;
   if (!x || !idx || !wq || !wk || !wv || !q_out || !k_cache || !v_cache) return HSA_STEP_ERR_NULL;
   const size_t align = dtype == HSA_STEP_BF16 ? 16 : 4;
@@ -119,6 +120,7 @@ int attention_core(int dtype, const void* q, const void* k_cache, const void* v_
       n_tokens > kMaxRows || (n_active > 0 && n_tokens < 1) || !(scale > 0.f) || !isfinite(scale))
     return HSA_STEP_ERR_SHAPE;
   if ((int64_t)heads * head_dim > INT32_MAX) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, (int64_t)heads * head_dim, es)) return HSA_STEP_ERR_SHAPE;
   if (n_active == 0) return HSA_STEP_OK;
   if (!q || !k_cache || !v_cache || !o) return HSA_STEP_ERR_NULL;
   const size_t align = dtype == HSA_STEP_BF16 ? 16 : 4;
@@ -170,6 +172,7 @@ HSA_API int hsa_out_scatter(int dtype, const void* o, const int32_t* idx, int32_
   if (d <= 0 || n_active < 0 || n_tokens < 0 || n_tokens > kMaxRows || n_active > n_tokens)
     return HSA_STEP_ERR_SHAPE;
   if (dtype == HSA_STEP_BF16 && d % 64 != 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, d, es) || !fits(d, d, es)) return HSA_STEP_ERR_SHAPE;
   if (n_active == 0) return HSA_STEP_OK;
   if (!o || !idx || !wo || !out) return HSA_STEP_ERR_NULL;
   const size_t align = dtype == HSA_STEP_BF16 ? 16 : 4;
@@ -219,6 +222,7 @@ HSA_API int hsa_active_attention(int dtype, const void* q, const void* k_cache,
     return HSA_STEP_ERR_SHAPE;
   const int32_t d = heads * head_dim;
   if (n_active < 0 || n_tokens < 0 || n_active > n_tokens) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, d, es) || !fits(d, d, es)) return HSA_STEP_ERR_SHAPE;
   if (n_active == 0) return HSA_STEP_OK;
   const size_t need = hsa_attention_workspace_bytes(dtype, n_active, d);
   if (!workspace || workspace_bytes < need) return HSA_STEP_ERR_WORKSPACE;
@@ -262,6 +266,7 @@ HSA_API int hsa_cached_euler(float* x, float* v_cache, const float* v_fresh, con
                              int32_t n_active, int64_t n_tokens, int32_t channels, float sigma_i,
                              float sigma_next, hipStream_t stream) {
   if (n_tokens < 0 || n_tokens > kMaxRows || channels < 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, channels, 4)) return HSA_STEP_ERR_SHAPE;
   if (v_fresh && (n_active < 0 || n_active > n_tokens)) return HSA_STEP_ERR_SHAPE;
   const size_t nb = (size_t)n_tokens * (size_t)channels * 4;
   if (nb == 0) return HSA_STEP_OK;

@@ -11,6 +11,9 @@ using namespace hsa_api;
 
 namespace {
 
+// Layers of one stack (the host arrays hold 4 and 2 pointers per layer).
+constexpr int kMaxLayers = 1 << 16;
+
 struct Span {
   const void* p;
   size_t n;
@@ -97,6 +100,7 @@ HSA_API int hsa_gather_rows(int dtype, const float* x, const int32_t* idx, int32
   if (!es) return HSA_STEP_ERR_DTYPE;
   if (n_active < 0 || n_tokens < 0 || n_tokens > kMaxRows || channels < 0)
     return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, channels, 4)) return HSA_STEP_ERR_SHAPE;
   if (n_active == 0 || channels == 0) return HSA_STEP_OK;
   if (!x || !idx || !xa) return HSA_STEP_ERR_NULL;
   if (!aligned(x, 4) || !aligned(idx, 4) || !aligned(xa, es)) return HSA_STEP_ERR_SHAPE;
@@ -113,6 +117,7 @@ HSA_API int hsa_row_rms_scale(int dtype, const void* x, int32_t n_rows, int32_t 
   const size_t es = elem_size(dtype);
   if (!es) return HSA_STEP_ERR_DTYPE;
   if (n_rows < 0 || d <= 0 || !(eps >= 0.f) || !isfinite(eps)) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_rows, d, es)) return HSA_STEP_ERR_SHAPE;
   if (n_rows == 0) return HSA_STEP_OK;
   if (!x || !scale) return HSA_STEP_ERR_NULL;
   if (!aligned(x, es) || !aligned(scale, 4)) return HSA_STEP_ERR_SHAPE;
@@ -130,6 +135,7 @@ HSA_API int hsa_linear(int dtype, const void* x, int32_t n_rows, int32_t d_in, c
     return HSA_STEP_ERR_DTYPE;
   const bool f32_out = dtype == HSA_STEP_BF16 && out_dtype == HSA_STEP_F32;
   if (n_rows < 0 || d_in <= 0 || d_out <= 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_rows, d_in, 4) || !fits(n_rows, d_out, 4) || !fits(d_out, d_in, 4)) return HSA_STEP_ERR_SHAPE;
   if ((f32_out || gelu) && residual) return HSA_STEP_ERR_SHAPE;
   if (f32_out && gelu) return HSA_STEP_ERR_SHAPE;
   if (dtype == HSA_STEP_BF16 && (d_in % 64 != 0 || d_out % 4 != 0)) return HSA_STEP_ERR_SHAPE;
@@ -158,6 +164,7 @@ HSA_API int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channel
                                int32_t n_groups, int32_t* budget, void* workspace,
                                size_t workspace_bytes, hipStream_t stream) {
   if (n_tokens < 0 || n_tokens > kMaxRows || channels < 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, channels, 4)) return HSA_STEP_ERR_SHAPE;
   hsa::GroupTable tab{};
   const int st = make_group_table(T, group_budget, group_size, n_groups, n_tokens, &tab);
   if (st != HSA_STEP_OK) return st;
@@ -177,7 +184,9 @@ HSA_API int hsa_assign_budgets(const float* v, int64_t n_tokens, int32_t channel
 HSA_API size_t hsa_rope_table_floats(int32_t head_dim, int32_t grid_f, int32_t grid_h,
                                      int32_t grid_w) {
   if (head_dim < 6 || head_dim % 2 || grid_f < 1 || grid_h < 1 || grid_w < 1) return 0;
-  return (size_t)(grid_f + grid_h + grid_w) * head_dim;
+  const int64_t rows = (int64_t)grid_f + grid_h + grid_w;
+  if (!fits(rows, head_dim, 4)) return 0;
+  return (size_t)rows * head_dim;
 }
 
 HSA_API int hsa_rope_table(float theta, int32_t head_dim, int32_t grid_f, int32_t grid_h,
@@ -237,6 +246,7 @@ HSA_API int hsa_reorder_plan(const int32_t* budget, int64_t n_tokens, int32_t T,
 HSA_API int hsa_permute_rows(const void* src, const int32_t* perm, int64_t n_rows, int64_t row_bytes,
                              int32_t inverse, void* dst, hipStream_t stream) {
   if (n_rows < 0 || n_rows > kMaxRows || row_bytes < 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_rows, row_bytes)) return HSA_STEP_ERR_SHAPE;
   if (n_rows == 0 || row_bytes == 0) return HSA_STEP_OK;
   if (!src || !perm || !dst) return HSA_STEP_ERR_NULL;
   if (!aligned(perm, 4)) return HSA_STEP_ERR_SHAPE;
@@ -251,6 +261,7 @@ HSA_API int hsa_l1_rel_accumulate(const float* v, float* v_prev, int64_t n_token
                                   int32_t channels, double* acc, int32_t first,
                                   hipStream_t stream) {
   if (n_tokens < 0 || n_tokens > kMaxRows || channels < 0) return HSA_STEP_ERR_SHAPE;
+  if (!fits(n_tokens, channels, 4)) return HSA_STEP_ERR_SHAPE;
   if (n_tokens == 0) return HSA_STEP_OK;
   if (!v || !v_prev || !acc) return HSA_STEP_ERR_NULL;
   if (!aligned(v, 4) || !aligned(v_prev, 4) || !aligned(acc, 8)) return HSA_STEP_ERR_SHAPE;
@@ -285,10 +296,16 @@ HSA_API int hsa_stack_iteration(const hsa_stack* s, int32_t T, int32_t iter, int
   const int64_t N = s->n_tokens;
   const int L = s->n_layers, C = s->channels, dh = s->head_dim;
   const int F = s->ffn_dim, Lc = s->ctx_len;
-  if (N < 1 || N > kMaxRows || L < 0 || s->heads <= 0 || (dh != 64 && dh != 128) || C <= 0 ||
-      s->reserved != 0 || s->reserved2 != 0 || (int64_t)s->heads * dh > INT32_MAX / 4 || F < 0 ||
-      Lc < 0 || Lc > kMaxRows)
+  if (N < 1 || N > kMaxRows || L < 0 || L > kMaxLayers || s->heads <= 0 || (dh != 64 && dh != 128) ||
+      C <= 0 || s->reserved != 0 || s->reserved2 != 0 || (int64_t)s->heads * dh > INT32_MAX / 4 ||
+      F < 0 || Lc < 0 || Lc > kMaxRows)
     return HSA_STEP_ERR_SHAPE;
+  {
+    const int64_t dd = (int64_t)s->heads * dh;
+    if (!fits(N, dd, 4) || !fits(N, C, 4) || !fits(N, F, 4) || !fits(dd, dd, 4) || !fits(F, dd, 4) ||
+        !fits(Lc, dd, 4) || !fits(C, dd, 4))
+      return HSA_STEP_ERR_SHAPE;
+  }
   const bool rope = s->rope_cs != nullptr;
   const bool prefix = s->prefix_cache != 0;
   if (s->reserved3 != 0 || (s->prefix_cache != 0 && s->prefix_cache != 1)) return HSA_STEP_ERR_SHAPE;

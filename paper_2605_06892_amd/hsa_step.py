@@ -184,13 +184,19 @@ def hsa_window_margin(center_percent: int, T: int) -> int:
 
 
 def hsa_build_active_set(budget, T: int, iteration: int, margin: int, idx, n_active_dev,
-                         read_back: bool = True, stream=None, outside_period: int = 1):
+                         read_back: bool = True, stream=None, outside_period: int = 1, host_buf=None):
     """Fill idx[:|A_i|] with the active set; returns |A_i| when read_back
     (one stream synchronization), else None. outside_period != 1 calls
-    hsa_build_active_set_window."""
+    hsa_build_active_set_window. host_buf: optional pinned int32 CPU tensor
+    of one element that receives the count (a direct DMA)."""
     _dev(budget, idx, n_active_dev)
     host = ctypes.c_int32(-2)
-    hb = ctypes.byref(host) if read_back else None
+    if host_buf is not None:
+        if host_buf.device.type != "cpu" or host_buf.dtype != torch.int32 or host_buf.numel() < 1:
+            raise ValueError("host_buf must be a CPU int32 tensor with at least one element")
+        hb = ctypes.c_void_p(host_buf.data_ptr()) if read_back else None
+    else:
+        hb = ctypes.byref(host) if read_back else None
     if outside_period == 1:
         fn = "hsa_build_active_set"
         st = lib().hsa_build_active_set(_ptr(budget), budget.numel(), T, iteration, margin, _ptr(idx),
@@ -200,7 +206,9 @@ def hsa_build_active_set(budget, T: int, iteration: int, margin: int, idx, n_act
         st = lib().hsa_build_active_set_window(_ptr(budget), budget.numel(), T, iteration, margin, outside_period,
                                                _ptr(idx), _ptr(n_active_dev), hb, _stream(stream))
     _check(fn, st)
-    return host.value if read_back else None
+    if not read_back:
+        return None
+    return int(host_buf[0]) if host_buf is not None else host.value
 
 
 def hsa_qkv_scatter(x, idx, n_active: int, wq, wk, wv, q_out, k_cache, v_cache,

@@ -43,6 +43,7 @@ class BlockBuffers:
     heads: int
     head_dim: int
     parts: torch.Tensor | None = None  # uint8 scratch: key parts of the attention launches
+    n_active_host: torch.Tensor | None = None  # pinned int32 [1]: the read-back of |A_i|
 
     @property
     def N(self) -> int:
@@ -70,13 +71,14 @@ class BlockBuffers:
         return cls(x=e(N, d), wq=e(d, d), wk=e(d, d), wv=e(d, d), wo=e(d, d),
                    k_cache=e(N, d), v_cache=e(N, d), out=e(N, d), q=e(N, d), o=e(N, d),
                    budget=e(N, dt=torch.int32), idx=e(N, dt=torch.int32),
-                   n_active=e(1, dt=torch.int32), heads=heads, head_dim=head_dim, parts=parts)
+                   n_active=e(1, dt=torch.int32), heads=heads, head_dim=head_dim, parts=parts,
+                   n_active_host=torch.empty(1, dtype=torch.int32, pin_memory=torch.device(device).type == "cuda"))
 
 
 def active_set(b: BlockBuffers, T: int, iteration: int, margin: int = 0, outside_period: int = 1) -> int:
     """A_i into b.idx; returns |A_i| (one stream synchronization)."""
     return H.hsa_build_active_set(b.budget, T, iteration, margin, b.idx, b.n_active,
-                                  outside_period=outside_period)
+                                  outside_period=outside_period, host_buf=b.n_active_host)
 
 
 def qkv(b: BlockBuffers, n_active: int, x_compact: bool = False) -> None:

@@ -47,3 +47,31 @@ def torch_dtype(dtype: str):
 
 
 TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+GUARD_BYTES = 64 << 10  # red zone before and after a guarded tensor
+
+
+class Guarded:
+    """A device tensor between two red zones of GUARD_BYTES bytes that hold a
+    seeded byte pattern. `t` is the tensor to pass to the library (256-byte
+    aligned, contiguous); check() fails if any byte of either red zone changed,
+    i.e. if a kernel wrote outside the buffer it was given."""
+
+    def __init__(self, shape, dtype, seed=0):
+        es = torch.empty((), dtype=dtype).element_size()
+        n = int(np.prod(shape)) * es
+        n_pad = (n + 255) // 256 * 256
+        self.raw = torch.empty(2 * GUARD_BYTES + n_pad, dtype=torch.uint8, device=DEV)
+        g = torch.Generator(device="cpu").manual_seed(seed)
+        self.pattern = torch.randint(0, 256, (GUARD_BYTES,), dtype=torch.uint8, generator=g).to(DEV)
+        self.raw[:GUARD_BYTES] = self.pattern
+        self.raw[GUARD_BYTES + n_pad:] = self.pattern
+        self.n_pad = n_pad
+        self.t = self.raw[GUARD_BYTES:GUARD_BYTES + n].view(dtype).view(*shape)
+
+    def check(self, name=""):
+        before = self.raw[:GUARD_BYTES]
+        after = self.raw[GUARD_BYTES + self.n_pad:]
+        assert torch.equal(before, self.pattern), f"write before the start of {name}"
+        assert torch.equal(after, self.pattern), f"write past the end of {name}"

@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import DEV, TOL, host, host_bits, i32, rel_inf, to_dev, torch_dtype
+from gpu_util import DEV, TOL, Guarded, host, host_bits, i32, rel_inf, to_dev, torch_dtype
 
 H = pytest.importorskip("paper_2605_06892_amd.hsa_step")
 
@@ -42,6 +42,8 @@ AS_CASES = [
     (32760, 40, (40, 20, 10, 5), (0, 3, 4, 5, 35, 36, 39), 4),
     (5000, 2000, (2000, 1000, 400, 1), (0, 1, 5, 1000, 1999), 0),   # T beyond the LDS table
     (3001, 12, (12, 6, 4, 3, 2, 1), range(12), 0),
+    (300001, 40, (40, 20, 10, 5), (0, 1, 2, 3), 0),  # 16 ranges of several 16384-token chunks each
+    (4097, 40, (40, 20, 10, 5), (1, 2), 0),          # two ranges, the second of one token
 ]
 
 
@@ -50,14 +52,18 @@ def test_active_set_bit_exact(case):
     N, T, budgets, its, margin = case
     b = _budgets(N, budgets, N + T)
     budget = i32(b)
-    idx = torch.full((max(N, 1),), -7, dtype=torch.int32, device=DEV)
-    cnt = torch.zeros(1, dtype=torch.int32, device=DEV)
+    gi, gc = Guarded((max(N, 1),), torch.int32, 3), Guarded((1,), torch.int32, 4)
+    idx, cnt = gi.t, gc.t
+    idx.fill_(-7)
+    cnt.zero_()
     for i in its:
         n = H.hsa_build_active_set(budget, T, i, margin, idx, cnt)
         ref = oracle.active_set(b, T, i, margin)
         assert n == ref.size
         assert int(cnt.item()) == n
         np.testing.assert_array_equal(idx[:n].cpu().numpy(), ref)
+        gi.check("idx")
+        gc.check("n_active")
 
 
 @pytest.mark.parametrize("N,T,budgets,margin,period", [(32760, 40, (20, 5), 4, 2), (5000, 40, (40, 10, 5), 10, 1),
@@ -151,9 +157,14 @@ def test_cached_euler_index_patterns(N, C):
     s = synth.linear_sigmas(40)
     for name, idx_np in _euler_patterns(N).items():
         st = synth.draw_euler_state(N, C, idx_np.size, seed=N * 7 + C)
-        x, vc = to_dev(st["x"], "f32"), to_dev(st["v_cache"], "f32")
+        gx, gv = Guarded((N, C), torch.float32, 1), Guarded((N, C), torch.float32, 2)
+        x, vc = gx.t, gv.t
+        x.copy_(to_dev(st["x"], "f32"))
+        vc.copy_(to_dev(st["v_cache"], "f32"))
         H.hsa_cached_euler(x, vc, to_dev(st["v_fresh"], "f32"), i32(idx_np), idx_np.size, float(s[3]),
                            float(s[4]))
+        gx.check("x")
+        gv.check("v_cache")
         x_ref, v_ref = oracle.cached_euler(st["x"], st["v_cache"], st["v_fresh"], idx_np, s[3], s[4])
         np.testing.assert_array_equal(host(vc), v_ref, err_msg=name)
         assert rel_inf(host(x), x_ref) <= 1e-6, name

@@ -24,7 +24,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import DEV, TOL, host, host_bits, i32, rel_inf, to_dev
+from gpu_util import DEV, TOL, Guarded, host, host_bits, i32, rel_inf, to_dev
 
 pytest.importorskip("paper_2605_06892_amd.hsa_step")
 from paper_2605_06892_amd import layer as L  # noqa: E402
@@ -82,6 +82,11 @@ def test_full_shape_iteration(name, it, layout):
     idx_ref = oracle.active_set(budget, wl.T, it)
 
     b = L.BlockBuffers.allocate(N, d, wl.heads, wl.dh, torch.bfloat16)
+    # every buffer the step writes sits between red zones
+    guards = {k: Guarded(tuple(getattr(b, k).shape), getattr(b, k).dtype, seed=i)
+              for i, k in enumerate(("k_cache", "v_cache", "out", "q", "o", "idx", "n_active"))}
+    for k, gz in guards.items():
+        setattr(b, k, gz.t)
     b.x.copy_(to_dev(blk["x"], "bf16"))
     for k in ("wq", "wk", "wv", "wo"):
         getattr(b, k).copy_(to_dev(blk[k], "bf16"))
@@ -95,6 +100,8 @@ def test_full_shape_iteration(name, it, layout):
     print(f"full-shape iteration {name} i={it} {layout}: |A|={n} of N={N}", flush=True)
     L.layer_step(b, n)
     torch.cuda.synchronize()
+    for k, gz in guards.items():
+        gz.check(k)
     if n == N:
         # all active: the identity index list, every output row written (none keeps its old
         # value) and finite
