@@ -22,7 +22,9 @@
 // construction. Budget validity and activity per budget value come from a
 // per-launch LDS table (T <= 1024), so the hot loop has no integer division.
 // The last workgroup has seen every token (its prefix and its own range), so
-// it alone writes |A_i|, or -1 if any budget is invalid.
+// it alone writes |A_i|, or -1 if any budget is invalid. All of a thread's
+// first global loads are issued before the LDS table is built and before any
+// of them is used, so the launch pays about one memory latency.
 #include "common.h"
 
 #include <algorithm>
@@ -58,7 +60,16 @@ __device__ __forceinline__ int block_sum(int v, int* red) {
 }
 
 // Workgroup b takes tokens [b * range, min(n, (b + 1) * range)); range is a
-// multiple of 4.
+// multiple of 4. Every global load a thread makes for the prefix count (up to
+// kPrefix int4 per thread per round) and for its first chunk is issued before
+// the LDS table is built, so their latencies overlap.
+constexpr int kPrefix = 8;  // prefix loads per thread per round: 32768 tokens per round
+
+__device__ __forceinline__ int4 load4(const int32_t* __restrict__ p, bool aligned) {
+  if (aligned) return *reinterpret_cast<const int4*>(p);
+  return make_int4(p[0], p[1], p[2], p[3]);
+}
+
 __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __restrict__ budget,
                                                               int n, int range, int T, int iter,
                                                               int margin, int outside_period,
@@ -70,6 +81,36 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
   const int w = t / kWave;
+  const bool aligned = (reinterpret_cast<uintptr_t>(budget) & 15) == 0;
+  const int r0 = (int)min((long)blockIdx.x * range, (long)n);
+  const int r1 = (int)min((long)r0 + range, (long)n);
+
+  // loads first: the first round of the prefix and the first chunk of the range
+  int4 pre[kPrefix];
+#pragma unroll
+  for (int q = 0; q < kPrefix; ++q) {
+    const int e = (q * kThreads + t) * 4;
+    pre[q] = e < r0 ? load4(budget + e, aligned) : make_int4(0, 0, 0, 0);
+  }
+  int b[kPer];
+  {
+    const int e0 = r0 + t * kPer;
+    if (aligned && e0 + kPer <= r1) {
+      const int4* p = reinterpret_cast<const int4*>(budget + e0);
+#pragma unroll
+      for (int r = 0; r < kPer / 4; ++r) {
+        const int4 v = p[r];
+        b[4 * r + 0] = v.x;
+        b[4 * r + 1] = v.y;
+        b[4 * r + 2] = v.z;
+        b[4 * r + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < kPer; ++r) b[r] = (e0 + r < r1) ? budget[e0 + r] : 0;
+    }
+  }
+
   const bool outside = margin > 0 && (iter < margin || iter > T - margin - 1);
   const bool outside_active = outside && (iter % outside_period) == 0;
   const bool use_table = T <= kMaxTableT;
@@ -83,50 +124,43 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
     return classify(s, T, iter, outside, outside_active);
   };
 
-  const bool aligned = (reinterpret_cast<uintptr_t>(budget) & 15) == 0;
-  const int r0 = (int)min((long)blockIdx.x * range, (long)n);
-  const int r1 = (int)min((long)r0 + range, (long)n);
   int bad = 0;
   // active tokens before this workgroup's range
   int before_me = 0;
   if (r0 > 0) {
     int cnt = 0;
-    for (int e = t * 4; e < r0; e += kThreads * 4) {  // r0 is a multiple of 4
-      int b4[4];
-      if (aligned) {
-        const int4 v = *reinterpret_cast<const int4*>(budget + e);
-        b4[0] = v.x; b4[1] = v.y; b4[2] = v.z; b4[3] = v.w;
-      } else {
+    auto count4 = [&](int4 v) {
+      const int c0 = cls_of(v.x), c1 = cls_of(v.y), c2 = cls_of(v.z), c3 = cls_of(v.w);
+      bad |= (c0 == 0) | (c1 == 0) | (c2 == 0) | (c3 == 0);
+      cnt += (c0 == 2) + (c1 == 2) + (c2 == 2) + (c3 == 2);
+    };
 #pragma unroll
-        for (int r = 0; r < 4; ++r) b4[r] = budget[e + r];
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c = cls_of(b4[r]);
-        bad |= (c == 0);
-        cnt += (c == 2);
-      }
-    }
+    for (int q = 0; q < kPrefix; ++q)
+      if ((q * kThreads + t) * 4 < r0) count4(pre[q]);
+    // further rounds (prefixes beyond 32768 tokens)
+    for (long e = (long)(kPrefix * kThreads + t) * 4; e < r0; e += kThreads * 4)
+      count4(load4(budget + e, aligned));
     before_me = block_sum(cnt, wave_total);
   }
 
   int base = before_me;  // active tokens before the current chunk
-  for (int c0 = r0; c0 < r1; c0 += kChunk) {
-    const int e0 = c0 + t * kPer;
-    int b[kPer];
-    if (aligned && e0 + kPer <= r1) {
-      const int4* p = reinterpret_cast<const int4*>(budget + e0);
+  for (long c0 = r0; c0 < r1; c0 += kChunk) {
+    const long e0 = c0 + t * kPer;
+    if (c0 != r0) {  // the first chunk was loaded above
+      if (aligned && e0 + kPer <= r1) {
+        const int4* p = reinterpret_cast<const int4*>(budget + e0);
 #pragma unroll
-      for (int r = 0; r < kPer / 4; ++r) {
-        int4 v = p[r];
-        b[4 * r + 0] = v.x;
-        b[4 * r + 1] = v.y;
-        b[4 * r + 2] = v.z;
-        b[4 * r + 3] = v.w;
+        for (int r = 0; r < kPer / 4; ++r) {
+          const int4 v = p[r];
+          b[4 * r + 0] = v.x;
+          b[4 * r + 1] = v.y;
+          b[4 * r + 2] = v.z;
+          b[4 * r + 3] = v.w;
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < kPer; ++r) b[r] = (e0 + r < r1) ? budget[e0 + r] : 0;
       }
-    } else {
-#pragma unroll
-      for (int r = 0; r < kPer; ++r) b[r] = (e0 + r < r1) ? budget[e0 + r] : 0;
     }
     unsigned mask = 0;
 #pragma unroll
@@ -156,7 +190,7 @@ __global__ __launch_bounds__(kThreads) void active_set_kernel(const int32_t* __r
     int pos = base + before + inc - cnt;
     while (mask) {
       const int r = __builtin_ctz(mask);
-      idx[pos++] = e0 + r;
+      idx[pos++] = (int32_t)(e0 + r);
       mask &= mask - 1;
     }
     base += total;
