@@ -549,3 +549,28 @@ def test_prefix_cache_equals_full_cache_bitwise(kv_parts, extra, monkeypatch):
     for (k0, v0), (k1, v1) in zip(full.caches, pre.caches):
         assert torch.equal(k0[:n_cached], k1) and torch.equal(v0[:n_cached], v1)
     assert torch.equal(full.caches[-1][0][n_cached:], pre.k_tail)  # the last layer's fresh baseline keys
+
+
+def test_refused_refresh_leaves_state_unchanged():
+    # a refresh iteration (every group's schedule fires, i = 4 for T = 8 and budgets {8, 4, 2}) where
+    # the budgets in force leave a token inactive is refused before anything changes the caller's state
+    wl = synth.WORKLOADS["tiny_stack_f32"]
+    N, L = wl.N, wl.layers
+    wts = synth.draw_stack(wl, seed=5)
+    st = _state_for(wl, 6, N, L)
+    st["budget"] = np.full(N, 4, np.int32)  # active at even iterations
+    st["budget"][17] = 1                    # active at i = 0 only
+    b = _upload(wl, wts, N, L, state=st)
+    sizes = synth.group_sizes(N, wl.groups)
+    sig = synth.linear_sigmas(wl.T)
+    before = [t.clone() for t in (b.x, b.v_hat, b.budget)] + [t.clone() for kv in b.caches for t in kv]
+    with pytest.raises(H.HsaStepError) as e:
+        S.iteration(b, wl.T, 4, sig, sizes)
+    assert e.value.name == "HSA_STEP_ERR_BUDGET"
+    torch.cuda.synchronize()
+    after = [b.x, b.v_hat, b.budget] + [t for kv in b.caches for t in kv]
+    for x0, x1 in zip(before, after):
+        assert torch.equal(x0, x1)
+    # the same state at a non-refresh iteration runs
+    n, refreshed = S.iteration(b, wl.T, 2, sig, sizes)
+    assert n == N - 1 and not refreshed
