@@ -19,11 +19,13 @@ H = pytest.importorskip("paper_2605_06892_amd.hsa_step")
 pytestmark = pytest.mark.gpu
 
 
-def to_dev(a, _dtype):
-    return torch.from_numpy(a).to(DEV).to(torch.bfloat16)
+DT = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 
-def _case(N, heads, dh, n_active, seed):
+def _case(N, heads, dh, n_active, seed, dtype="bf16"):
+    def to_dev(a, _tag):
+        return torch.from_numpy(a).to(DEV).to(DT[dtype])
+
     rng = np.random.default_rng(seed)
     d = heads * dh
     idx = np.sort(rng.choice(N, size=n_active, replace=False)).astype(np.int32)
@@ -42,7 +44,7 @@ def _both(t, heads, dh):
     n_active = t["q"].shape[0]
     scale = 1.0 / np.sqrt(dh)
     # the caller-workspace entry point, with room for every key-part split (as the fixed array has)
-    nb = H.hsa_attention_parts_workspace_bytes(torch.bfloat16, n_active, heads, dh)
+    nb = H.hsa_attention_parts_workspace_bytes(t["q"].dtype, n_active, heads, dh)
     ws = torch.empty(nb, dtype=torch.uint8, device=DEV)
     out_a = t["out0"].clone()
     H.hsa_active_attention(t["q"], t["k"], t["v"], t["idx"], n_active, heads, dh, scale, t["wo"], out_a, ws)
@@ -52,12 +54,13 @@ def _both(t, heads, dh):
     return out_a, out_b
 
 
-@pytest.mark.parametrize("shape", [(4096, 8, 128, 1500, 300), (3000, 2, 64, 900, 77)], ids=str)
+@pytest.mark.parametrize("shape", [(4096, 8, 128, 1500, 300, "bf16"), (3000, 2, 64, 900, 77, "bf16"),
+                                   (2000, 4, 64, 700, 50, "f32")], ids=str)
 def test_noalloc_equals_workspace_entry_point(shape):
-    N, heads, dh, n1, n2 = shape
+    N, heads, dh, n1, n2, dtype = shape
     for n_active, seed in ((n1, 1), (n2, 2)):  # two calls in a row, the second smaller
-        print(f"noalloc attention N={N} heads={heads} dh={dh} n_active={n_active}", flush=True)
-        t = _case(N, heads, dh, n_active, seed + N)
+        print(f"noalloc attention {dtype} N={N} heads={heads} dh={dh} n_active={n_active}", flush=True)
+        t = _case(N, heads, dh, n_active, seed + N, dtype)
         out_a, out_b = _both(t, heads, dh)
         np.testing.assert_array_equal(host_bits(out_b), host_bits(out_a))
         # rows outside the active set untouched
