@@ -171,6 +171,27 @@ def test_cached_euler_index_patterns(N, C):
         assert np.mean(host(x) == x_ref) > 0.9999, name
 
 
+@pytest.mark.parametrize("pattern", ["random", "run"])
+def test_cached_euler_runs_of_tiles(pattern):
+    # enough token tiles (16 rows of 256 channels each, 18751 tiles) that the launch takes runs of
+    # 4 consecutive tiles per search
+    N, C = 300001, 256
+    idx_np = _euler_patterns(N)[pattern]
+    st = synth.draw_euler_state(N, C, idx_np.size, seed=77)
+    s = synth.linear_sigmas(40)
+    gx, gv = Guarded((N, C), torch.float32, 5), Guarded((N, C), torch.float32, 6)
+    x, vc = gx.t, gv.t
+    x.copy_(to_dev(st["x"], "f32"))
+    vc.copy_(to_dev(st["v_cache"], "f32"))
+    H.hsa_cached_euler(x, vc, to_dev(st["v_fresh"], "f32"), i32(idx_np), idx_np.size, float(s[5]), float(s[6]))
+    gx.check("x")
+    gv.check("v_cache")
+    x_ref, v_ref = oracle.cached_euler(st["x"], st["v_cache"], st["v_fresh"], idx_np, s[5], s[6])
+    np.testing.assert_array_equal(host(vc), v_ref)
+    assert rel_inf(host(x), x_ref) <= 1e-6
+    assert np.mean(host(x) == x_ref) > 0.9999
+
+
 def test_cached_euler_fp32_step_difference():
     # the shared step is sigma_next - sigma_i taken in fp32
     x = torch.zeros(4, 4, device=DEV)
