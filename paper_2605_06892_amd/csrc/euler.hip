@@ -9,8 +9,8 @@
 // locates the first fresh row of a run of tiles in the index list; from there
 // each tile's fresh rows are the next entries of the list (ascending), whose
 // positions go into an LDS slot table of the tile (double-buffered and tagged
-// with the tile number, so one barrier per tile suffices). Without fresh velocities
-// it is a plain stream x = fmaf(v_cache, dsig, x).
+// with the tile number, so one barrier per tile suffices). Without fresh
+// velocities it is a plain stream x = fmaf(v_cache, dsig, x).
 // Both are HBM-bound element streams: 16-byte nontemporal vector accesses when
 // the rows allow it, each thread keeping U independent 16-byte loads of each
 // input in flight before its stores.
@@ -105,10 +105,11 @@ __global__ __launch_bounds__(kThreads) void cached_euler_fused(
       for (int k0 = 0; k0 < rows; k0 += kThreads) {
         const int k = k0 + tid;
         bool in = false;
-        if (k < rows && j0 + k < n_active) {
-          const long t = idx[j0 + k];
+        const long j = (long)j0 + k;  // 64-bit: j0 may lie near 2^31
+        if (k < rows && j < n_active) {
+          const long t = idx[j];
           in = t >= t0 && t < t1;
-          if (in) sl[t - t0] = make_int2((int)tile, j0 + k);
+          if (in) sl[t - t0] = make_int2((int)tile, (int)j);
         }
         cnt += __syncthreads_count(in);
       }
