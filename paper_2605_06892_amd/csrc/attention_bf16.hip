@@ -50,7 +50,7 @@
 //                 one channel of 4 keys.
 // Software pipeline: the S^T MFMAs of block b+1 are issued next to the
 // exp2/sum instructions of block b (they are independent), then the PV MFMAs
-// of block b, next to the LDS reads of most K fragments of block b+2. Every
+// of block b, next to the LDS reads of half the K fragments of block b+2. Every
 // lane owns one query column in both S^T and O^T, so the softmax statistics
 // never need to be broadcast across lanes.
 #include "common.h"
@@ -227,9 +227,11 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
   bool have_ref = false;     // becomes true after the first 32 keys (wave-uniform)
   // K fragments 0..KP-1 of the block whose scores the next step computes,
   // read one step ahead (during the previous block's PV): the S^T MFMAs of a
-  // block then start without waiting on LDS. Six of the eight measured best
-  // (2% over none; all eight need 252 registers and lose 1%).
-  constexpr int KP = KK < 6 ? KK : 6;
+  // block then start without waiting on LDS. Four, together with the V
+  // fragments of head-dim tile 0 read before the softmax (below), measured
+  // best: 2-3% over no read-ahead; all eight K fragments need 252 registers
+  // and gain less.
+  constexpr int KP = KK < 4 ? KK : 4;
   bf16x8 kpre[KP];
   auto kfrag = [&](auto buf, int kb, int kk) {
     return *reinterpret_cast<const bf16x8*>(kbuf(buf) + kb * DH + koff[kk]);
@@ -262,6 +264,19 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
         if (kbase + (e >> 2) * 8 + (e & 3) >= kv_end) s_cur[e] = -INFINITY;
     }
     scores(nbuf, nkb, s_nxt);
+    const bf16* vbase = vbuf(buf) + vb * DH;
+    constexpr int NV = 1;  // head-dim tiles whose V fragments are read before the softmax
+                           // (their latency then hides behind it)
+    bf16x8 vfa[NV][2];
+#pragma unroll
+    for (int dt = 0; dt < NV; ++dt)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16* src = vbase + ks * 16 * DH + voff[dt];
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src + 8 * DH));
+        vfa[dt][ks] = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
     float p[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(s_cur[e]);
@@ -302,15 +317,19 @@ __global__ __launch_bounds__(NW * 64) void attention_bf16_kernel(
     }
 #pragma unroll
     for (int kk = 0; kk < KP; ++kk) kpre[kk] = kfrag(nnbuf, nnkb, kk);
-    const bf16* vbase = vbuf(buf) + vb * DH;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16* src = vbase + ks * 16 * DH + voff[dt];
-        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src));
-        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src + 8 * DH));
-        const bf16x8 vf = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        bf16x8 vf;
+        if (dt < NV) {
+          vf = vfa[dt][ks];
+        } else {
+          const bf16* src = vbase + ks * 16 * DH + voff[dt];
+          const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src));
+          const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(src + 8 * DH));
+          vf = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
         acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], acc[dt], 0, 0, 0);
       }
     }
