@@ -58,6 +58,16 @@ __device__ __forceinline__ void static_for(F&& f) {
 // GELU of the product.
 enum Epilogue { kEpiBf16 = 0, kEpiBf16Residual = 1, kEpiF32 = 2, kEpiBf16Gelu = 3 };
 
+// 16 bytes per lane from base + voff + soff, a buffer resource over the
+// nbytes bytes from base, straight into LDS at dst (the wave's 1 KB segment).
+// Against 64-bit lane pointers this needs no per-load address arithmetic and
+// half the registers; a load past nbytes reads zeros instead of faulting.
+__device__ __forceinline__ void buffer_load_lds16(const void* base, unsigned nbytes, bf16* dst, unsigned voff,
+                                                  unsigned soff) {
+  const auto r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)nbytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, soff, 0, 0);
+}
+
 // One tiling of the kernel: BM x BN output tile, K step BK (32 or 64),
 // STAGES LDS stages (loads run STAGES-1 steps ahead), WAVES waves in a
 // WM x (WAVES/WM) grid.
@@ -87,7 +97,9 @@ struct Tiling {
 // workgroup's LDS arrays L0..L3 (at least TL::STAGE elements each, as many as
 // TL has stages). Each stage is its own array, so that the compiler can tell
 // the asynchronous loads into one stage from the fragment reads of another.
-template <class TL, int EPI, class LA, class LB, class LC, class LD>
+// BUF: stage loads through buffer resources (A and B each below 4 GiB), else
+// through 64-bit lane pointers.
+template <class TL, int EPI, bool BUF, class LA, class LB, class LC, class LD>
 __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, int z, LA& L0, LB& L1,
                                               LC& L2, LD& L3) {
   constexpr int BM = TL::BM, BN = TL::BN, BK = TL::BK, STAGES = TL::STAGES, WN = TL::WN;
@@ -113,8 +125,9 @@ __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, 
   // tile rows SEG_ROWS*s .. (A tile first, then B tile); the lane fetches
   // row SEG_ROWS*s + lane/CHUNKS, global chunk (lane%CHUNKS) ^ swz(row),
   // into LDS slot lane%CHUNKS.
-  const bf16* src[LOADS];
-  int dst[LOADS];  // element offset of the segment in its stage
+  const bf16* src[LOADS];  // !BUF: the lane's chunk of its row in A or B
+  unsigned voff[LOADS];    // BUF: the same as a byte offset from A or B
+  int dst[LOADS];          // element offset of the segment in its stage
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
     const int s = i * TL::WAVES + wave;
@@ -131,13 +144,27 @@ __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, 
       const int n = min(tn * BN + trow, g.Nc - 1);
       grow = (long)n * g.ldb;
     }
-    src[i] = (a ? A : B) + grow + chunk * 8;
+    if constexpr (BUF)
+      voff[i] = (unsigned)((grow + chunk * 8) * 2);
+    else
+      src[i] = (a ? A : B) + grow + chunk * 8;
     dst[i] = s * 512;  // the B tile follows the A tile in the stage
   }
-  auto issue = [&](auto st, int k0) {
+  // segment i of every wave lies in A when i * WAVES < SEG_A (SEG_A is a
+  // multiple of WAVES), so the resource of a load is known at compile time
+  const unsigned a_bytes = (unsigned)((long)g.a_limit * g.lda * 2), b_bytes = (unsigned)((long)g.Nc * g.ldb * 2);
+  auto issue = [&](auto st, int k0) -> void {
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i)
-      __builtin_amdgcn_global_load_lds((global_cvoid*)(src[i] + k0), (lds_void*)(stage(st) + dst[i]), 16, 0, 0);
+    for (int i = 0; i < LOADS; ++i) {
+      if constexpr (BUF) {
+        if (i * TL::WAVES < SEG_A)
+          buffer_load_lds16(A, a_bytes, stage(st) + dst[i], voff[i], (unsigned)(k0 * 2));
+        else
+          buffer_load_lds16(B, b_bytes, stage(st) + dst[i], voff[i], (unsigned)(k0 * 2));
+      } else {
+        __builtin_amdgcn_global_load_lds((global_cvoid*)(src[i] + k0), (lds_void*)(stage(st) + dst[i]), 16, 0, 0);
+      }
+    }
   };
 
   // fragment read offsets: row (tile-local) l32 + 32*t, chunk kk*2 + hi;
@@ -388,7 +415,7 @@ using TMid = Tiling<256, 128, 64, 2, 8, 4>;
 // halves of the tile workgroup split_from + j would have taken. The launcher
 // sets split_from so that a last, partly filled round of big tiles becomes
 // one round of halves.
-template <class TL, int NOUT, int EPI>
+template <class TL, int NOUT, int EPI, bool BUF>
 __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   constexpr int STAGES = TL::STAGES;
   constexpr bool kSplit = std::is_same<TL, TBig>::value;
@@ -420,11 +447,11 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   const int tn = tnc - z * tiles_n1;
   if constexpr (kSplit) {
     if (half >= 0) {
-      row_gemm_tile<TMid, EPI>(g, tm, tn * 2 + half, z, L0, L1, L2, L3);
+      row_gemm_tile<TMid, EPI, BUF>(g, tm, tn * 2 + half, z, L0, L1, L2, L3);
       return;
     }
   }
-  row_gemm_tile<TL, EPI>(g, tm, tn, z, L0, L1, L2, L3);
+  row_gemm_tile<TL, EPI, BUF>(g, tm, tn, z, L0, L1, L2, L3);
 }
 
 // Rounds of a launch of `tiles` tiles on the CUs, in units of a full round
@@ -456,7 +483,12 @@ hipError_t launch(const RowGemm& g0, hipStream_t s) {
     g.split_from = (int)(tiles - rem);
     grid = tiles + rem;
   }
-  hipLaunchKernelGGL((row_gemm_bf16_kernel<TL, NOUT, EPI>), dim3((unsigned)grid), dim3(TL::THREADS), 0, s, g);
+  // buffer resources address 4 GiB - 1 bytes from their base (32-bit offsets)
+  const long lim = 0xffffffffL;
+  if ((long)g.a_limit * g.lda * 2 <= lim && (long)g.Nc * g.ldb * 2 <= lim)
+    hipLaunchKernelGGL((row_gemm_bf16_kernel<TL, NOUT, EPI, true>), dim3((unsigned)grid), dim3(TL::THREADS), 0, s, g);
+  else
+    hipLaunchKernelGGL((row_gemm_bf16_kernel<TL, NOUT, EPI, false>), dim3((unsigned)grid), dim3(TL::THREADS), 0, s, g);
   return hipGetLastError();
 }
 
