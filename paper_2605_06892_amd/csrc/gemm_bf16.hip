@@ -10,15 +10,17 @@
 //
 // Tiling (struct Tiling): BM x BN output tile per workgroup of 8 waves in a
 // WM x WN grid, K step 64, v_mfma_f32_32x32x16_bf16. Tiles go global -> LDS
-// directly (global_load_lds_dwordx4: one wave instruction fills one
-// contiguous 1 KB segment = 8 tile rows of 128 bytes) into two stages, the
+// directly (buffer_load_dwordx4 ... lds through one buffer resource over A
+// and one over B, or global_load_lds_dwordx4 with 64-bit lane pointers for a
+// matrix of 4 GiB or more: one wave instruction fills one contiguous 1 KB
+// segment = 8 tile rows of 128 bytes) into two stages, the
 // loads of step k+1 in flight during the MFMAs of step k, one barrier per
 // step. Within a step the fragment reads of k slice s+1 and the stage loads
 // are placed one per MFMA between the MFMAs of slice s, so neither the LDS
 // latency nor the load issue stalls the matrix pipe (measured: issuing them
-// in bursts ahead of the MFMAs cost 5-10%), and the MFMAs of (some of) the
-// last slice's fragment rows run behind the next step's barrier, where they
-// cover that step's first reads (1-4%). The 16-byte chunks of tile row r
+// in bursts ahead of the MFMAs cost 5-10%), and the MFMAs of the last
+// slice's fragment rows (half of them at 256 x 256 with 64-bit pointers) run
+// behind the next step's barrier, where they cover that step's first reads. The 16-byte chunks of tile row r
 // sit at slot chunk ^ ((r >> 1) & 7), which keeps the fragment reads (16
 // rows, one chunk) on disjoint banks. Each stage is its own LDS array and the
 // K loop is unrolled by the stage count, so the compiler can tell the
