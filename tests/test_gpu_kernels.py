@@ -242,6 +242,38 @@ def test_qkv_scatter(dtype, N, d, frac, compact):
     assert rel_inf(host(vc)[idx_np], ref["v"]) <= tol
 
 
+def test_qkv_scatter_beyond_4gib():
+    """x, K_hat and V_hat of more than 4 GiB each (N = 2^20 + 64 rows of 2048
+    bf16): byte offsets pass 32 bits, so the GEMM launcher takes its 64-bit
+    lane-pointer load path instead of the buffer resources. The active rows
+    include the last 64 rows of x (offsets past 2^32); only active rows of x
+    are ever read, so only they hold drawn values."""
+    nA, d = 8190, 2048
+    N = (1 << 20) + 64
+    assert N * d * 2 > 0xFFFFFFFF
+    blk = _block(nA, d, "bf16", seed=4242)  # the active rows of x and the weights
+    rng = np.random.default_rng(4242)
+    idx_np = np.sort(np.concatenate([rng.choice(N - 64, nA - 64, replace=False), np.arange(N - 64, N)]))
+    ii = torch.from_numpy(idx_np).to(DEV)
+    x = torch.zeros(N, d, dtype=torch.bfloat16, device=DEV)
+    x[ii] = to_dev(blk["x"], "bf16")
+    w = {k: to_dev(blk[k], "bf16") for k in ("wq", "wk", "wv")}
+    kc = torch.zeros(N, d, dtype=torch.bfloat16, device=DEV)
+    vc = torch.zeros(N, d, dtype=torch.bfloat16, device=DEV)
+    q = torch.full((nA, d), 3.0, dtype=torch.bfloat16, device=DEV)
+    H.hsa_qkv_scatter(x, i32(idx_np), nA, w["wq"], w["wk"], w["wv"], q, kc, vc)
+    torch.cuda.synchronize()
+    assert rel_inf(host(q), oracle.project(blk["x"], blk["wq"], "bf16")) <= 1e-2
+    assert rel_inf(host(kc[ii]), oracle.project(blk["x"], blk["wk"], "bf16")) <= 1e-2
+    assert rel_inf(host(vc[ii]), oracle.project(blk["x"], blk["wv"], "bf16")) <= 1e-2
+    # rows outside A keep their (zero) contents: the tail region and a sample
+    skip = np.setdiff1d(np.concatenate([np.arange(N - 4096, N), rng.choice(N, 4096, replace=False)]), idx_np)
+    si = torch.from_numpy(skip).to(DEV)
+    assert int(torch.count_nonzero(kc[si])) == 0 and int(torch.count_nonzero(vc[si])) == 0
+    del x, kc, vc
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("N,d", [(5000, 512), (777, 128)])
 def test_identity_weights_gather_scatter_bit_exact(N, d):
     """Wq = Wk = Wv = I: the product is exact, so Q == x[A], K_hat[A] == V_hat[A]
