@@ -105,7 +105,8 @@ struct RowGemm {
   int gelu;                // apply the tanh GELU after the row scale (no residual)
   // Rotary embedding of the outputs z with bit z of rope_outs set: row m is
   // token rope_tok[m] at grid position p = rope_pos[token] (the token itself
-  // if null; outside [0, F*H*W) reads as 0), coordinates (p / (H*W),
+  // if null; outside [0, F*H*W) reads as 0; both are read for every m < M,
+  // stored or not), coordinates (p / (H*W),
   // (p / W) % H, p % W). Channel pair k of a head of rope_dh channels lies in
   // the temporal band (k < nt), the row band (k < nt + nh) or the column
   // band; its (cos, sin) is rope_cs[r * rope_dh/2 + k] with r the frame,
@@ -132,13 +133,21 @@ __device__ __forceinline__ RopeRow rope_row(const RowGemm& g, int m) {
   return {p / hw, (p / g.rope_w) % g.rope_h, p % g.rope_w};
 }
 
+// (cos, sin) of head-local channel pair k (0 <= k < rope_dh/2) of a row at
+// grid coordinates r; always an entry of the table.
+__device__ __forceinline__ f32x2 rope_angle(const RowGemm& g, const RopeRow& r, int k) {
+  const int row = k < g.rope_nt ? r.f
+                  : (k < g.rope_nt + g.rope_nh ? g.rope_f + r.y : g.rope_f + g.rope_h + r.x);
+  return g.rope_cs[row * (g.rope_dh >> 1) + k];
+}
+// The channel pair (a, b) rotated by the angle with (cos, sin) = cs.
+__device__ __forceinline__ f32x2 rope_rotate(f32x2 cs, float a, float b) {
+  return (f32x2){a * cs[0] - b * cs[1], a * cs[1] + b * cs[0]};
+}
 // The channel pair (a, b) at head-local pair index k, rotated.
 __device__ __forceinline__ f32x2 rope_pair(const RowGemm& g, const RopeRow& r, int k, float a,
                                            float b) {
-  const int row = k < g.rope_nt ? r.f
-                  : (k < g.rope_nt + g.rope_nh ? g.rope_f + r.y : g.rope_f + g.rope_h + r.x);
-  const f32x2 cs = g.rope_cs[row * (g.rope_dh >> 1) + k];
-  return (f32x2){a * cs[0] - b * cs[1], a * cs[1] + b * cs[0]};
+  return rope_rotate(rope_angle(g, r, k), a, b);
 }
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s);
 

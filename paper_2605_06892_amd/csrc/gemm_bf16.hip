@@ -100,8 +100,9 @@ struct Tiling {
 // TL has stages). Each stage is its own array, so that the compiler can tell
 // the asynchronous loads into one stage from the fragment reads of another.
 // BUF: stage loads through buffer resources (A and B each below 4 GiB), else
-// through 64-bit lane pointers.
-template <class TL, int EPI, bool BUF, class LA, class LB, class LC, class LD>
+// through 64-bit lane pointers. ROPE: the RoPE epilogue is compiled in (the
+// Q/K/V projection only).
+template <class TL, int EPI, bool BUF, bool ROPE, class LA, class LB, class LC, class LD>
 __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, int z, LA& L0, LB& L1,
                                               LC& L2, LD& L3) {
   constexpr int BM = TL::BM, BN = TL::BN, BK = TL::BK, STAGES = TL::STAGES, WN = TL::WN;
@@ -305,71 +306,113 @@ __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, 
   // of one row, so direct stores would write 16-byte pieces of 32 rows per
   // instruction. Instead, for each 32-row block i, every wave writes its
   // fp32 values (row scale, RoPE and GELU applied) to its own LDS region,
-  // then reads them back row-contiguous and stores runs of 4 columns per
-  // lane, 128 bytes or more per row (the residual is added there, then the
-  // value rounded once). Waves 0-3 use the first stage's array, 4-7 the
-  // second; the scatter target of each row travels through LDS too.
+  // then reads them back row-contiguous, 4 columns per lane (the residual is
+  // added there, then the value rounded once), and stores runs of 4 columns
+  // per lane, 128 bytes or more per row. Waves 0-3 use the first stage's
+  // array, 4-7 the second; the scatter target of each row travels through
+  // LDS too. Every global load of the epilogue (row indices, row scales,
+  // RoPE positions and angles, residuals) precedes its first store: the
+  // results of all blocks are held in registers and stored after the last
+  // one. A wave waits for a load by counting its outstanding memory
+  // accesses, stores included, so a load behind a store would also wait for
+  // that store (per block, this cost the Q/K/V projection about 10%).
   constexpr int TNP = TN + 4;         // padded staging row, floats
   constexpr int QPR = TN / 4;         // 4-column groups per row
-  constexpr int REGION = 32 * TNP * 4 + 32 * 8 + 32 * 4;
+  constexpr int NT = QPR / 2;         // read-back passes of the wave per block
+  constexpr int REGION = 32 * TNP * 4 + MI * 32 * (8 + 4);
   static_assert(4 * REGION <= TL::STAGE * 2, "epilogue staging must fit in a stage");
   static_assert(QPR % 2 == 0, "the wave covers whole rows in each read-back pass");
   __syncthreads();  // every wave is done with the stages
   char* region = reinterpret_cast<char*>((wave < 4) ? L0 : L1) + (wave % 4) * REGION;
   float* blk = reinterpret_cast<float*>(region);
-  long* row_off = reinterpret_cast<long*>(region + 32 * TNP * 4);   // output element offset
-  int* row_buf = reinterpret_cast<int*>(region + 32 * TNP * 4 + 32 * 8);  // 0: C, 1: C2, -1: none
+  // per block i, row r: output element offset and target (0: C, 1: C2, -1: none)
+  long* row_off = reinterpret_cast<long*>(region + 32 * TNP * 4);
+  int* row_buf = reinterpret_cast<int*>(region + 32 * TNP * 4 + MI * 32 * 8);
   const int32_t* c_rows = oz.c_rows;
-  const bool rope = g.rope_cs && ((g.rope_outs >> z) & 1);
+  const bool rope = ROPE && g.rope_cs && ((g.rope_outs >> z) & 1);
   const int col0 = tn * BN + wn * TN;  // first output column of the wave tile
+  const int m0 = tm * BM + wm * TM + l32;  // the lane's row in block 0
+  int crow[MI];
+  float rs[MI];
+  RopeRow rr[MI];
+  // Loads under a lane condition would each be waited for inside their
+  // branch, one after the other: every load here and below reads a valid
+  // address unconditionally (row M-1 for the rows past M) and its value is
+  // selected afterwards.
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
-    const int m = tm * BM + wm * TM + i * 32 + l32;
+    const int m = m0 + i * 32;
+    const int mc = min(m, g.M - 1);
+    const int cr = c_rows ? c_rows[mc] : m;
+    crow[i] = m < g.M ? cr : -1;
+    rs[i] = g.row_scale ? g.row_scale[mc] : 1.f;
+    rr[i] = RopeRow{0, 0, 0};
+    if (rope) rr[i] = rope_row(g, mc);
+  }
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
     int buf = -1;
     long obase = 0;
-    if (m < g.M) {
-      const int crow = c_rows ? c_rows[m] : m;
-      if (crow >= 0 && crow < oz.c_limit) {
-        const bool second = oz.C2 && crow >= oz.c_split;  // rows past the split go to C2
-        buf = second ? 1 : 0;
-        obase = (long)(second ? crow - oz.c_split : crow) * g.ldc;
-      }
+    if (crow[i] >= 0 && crow[i] < oz.c_limit) {
+      const bool second = oz.C2 && crow[i] >= oz.c_split;  // rows past the split go to C2
+      buf = second ? 1 : 0;
+      obase = (long)(second ? crow[i] - oz.c_split : crow[i]) * g.ldc;
     }
     if (hi == 0) {
-      row_off[l32] = obase;
-      row_buf[l32] = buf;
+      row_off[i * 32 + l32] = obase;
+      row_buf[i * 32 + l32] = buf;
     }
-    // The residual may be the output itself (h += ...), so the compiler
-    // cannot move a pass's residual load above the previous pass's store: all
-    // of the block's residual loads are issued here, before the staging
-    // writes, whose work then covers their latency.
-    bf16x4 res[QPR / 2];
-    if constexpr (EPI == kEpiBf16Residual) {
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // the row table is visible
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // the row tables are visible
+  typedef typename std::conditional<EPI == kEpiF32, f32x4, bf16x4>::type OutT;
+  OutT ov[MI][NT];  // block i, read-back pass t: the lane's 4 output values
 #pragma unroll
-      for (int t = 0; t < QPR / 2; ++t) {
+  for (int i = 0; i < MI; ++i) {
+    if constexpr (EPI == kEpiBf16Residual) {  // the residual first takes the output's place
+      __builtin_amdgcn_sched_barrier(0);  // one block's residuals at a time (registers)
+      bool in[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
         const int f = lane + 64 * t;
         const int r = f / QPR, cq = f - r * QPR;
         const int n = col0 + cq * 4;
-        res[t] = (bf16x4){};
-        if (row_buf[r] >= 0 && n < g.Nc)
-          res[t] = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) + row_off[r] + n);
+        in[t] = row_buf[i * 32 + r] >= 0 && n < g.Nc;
+        // element 0 of the residual exists: the launcher runs no residual
+        // product without output rows
+        ov[i][t] = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.residual) +
+                                                    (in[t] ? row_off[i * 32 + r] + n : 0));
+      }
+      // an empty asm that uses every value keeps the loads unconditional (the
+      // compiler would otherwise move each into a branch of its own)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        asm volatile("" : "+v"(ov[i][t]));
+        if (!in[t]) ov[i][t] = (bf16x4){};
       }
     }
-    const float rs = (g.row_scale && m < g.M) ? g.row_scale[m] : 1.f;
-    RopeRow rr{0, 0, 0};
-    if (rope && buf >= 0) rr = rope_row(g, m);
+    // the block's RoPE angles, all loaded before any is used (every index is
+    // in the table, so the loads need no condition)
+    f32x2 cs[NI][4][2];
+    if (rope) {
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int k = ((col0 + j * 32 + q * 8 + hi * 4) % g.rope_dh) >> 1;
+          cs[j][q][0] = rope_angle(g, rr[i], k);
+          cs[j][q][1] = rope_angle(g, rr[i], k + 1);
+        }
+    }
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int c = j * 32 + q * 8 + hi * 4;
         f32x4 v = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-        if (g.row_scale) v *= rs;
-        if (rope && buf >= 0 && col0 + c < g.Nc) {
-          const int k = ((col0 + c) % g.rope_dh) >> 1;
-          const f32x2 r0 = rope_pair(g, rr, k, v[0], v[1]);
-          const f32x2 r1 = rope_pair(g, rr, k + 1, v[2], v[3]);
+        if (g.row_scale) v *= rs[i];
+        if (rope) {
+          const f32x2 r0 = rope_rotate(cs[j][q][0], v[0], v[1]);
+          const f32x2 r1 = rope_rotate(cs[j][q][1], v[2], v[3]);
           v = (f32x4){r0[0], r0[1], r1[0], r1[1]};
         }
         if constexpr (EPI == kEpiBf16Gelu) {
@@ -380,26 +423,38 @@ __device__ __forceinline__ void row_gemm_tile(const RowGemm& g, int tm, int tn, 
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    // row-contiguous read-back: 4 columns per lane, QPR lanes per row, QPR/2
-    // passes of the wave
+    // row-contiguous read-back: 4 columns per lane, QPR lanes per row
 #pragma unroll
-    for (int t = 0; t < QPR / 2; ++t) {
+    for (int t = 0; t < NT; ++t) {
       const int f = lane + 64 * t;
       const int r = f / QPR, cq = f - r * QPR;
-      const int rb = row_buf[r];
-      const int n = col0 + cq * 4;
-      if (rb < 0 || n >= g.Nc) continue;
       f32x4 v = *reinterpret_cast<const f32x4*>(blk + r * TNP + cq * 4);
-      void* cbase = rb ? oz.C2 : oz.C;
-      const long o = row_off[r] + n;
       if constexpr (EPI == kEpiF32) {
-        *reinterpret_cast<f32x4*>(static_cast<float*>(cbase) + o) = v;
+        ov[i][t] = v;
       } else {
-        if constexpr (EPI == kEpiBf16Residual) v += __builtin_convertvector(res[t], f32x4);
-        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(cbase) + o) = to_bf16x4(v);
+        if constexpr (EPI == kEpiBf16Residual) v += __builtin_convertvector(ov[i][t], f32x4);
+        ov[i][t] = to_bf16x4(v);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // reads done before the next block's writes
+  }
+  // the stores read their targets from the row tables again (a compiler-only
+  // barrier): kept from the residual loads, 64-bit offsets would fill 64
+  // registers and spill
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int f = lane + 64 * t;
+      const int r = f / QPR, cq = f - r * QPR;
+      const int rb = row_buf[i * 32 + r];
+      const int n = col0 + cq * 4;
+      if (rb < 0 || n >= g.Nc) continue;
+      const long o = row_off[i * 32 + r] + n;
+      *reinterpret_cast<OutT*>(static_cast<typename std::conditional<EPI == kEpiF32, float, bf16>::type*>(
+          rb ? oz.C2 : oz.C) + o) = ov[i][t];
+    }
   }
 }
 
@@ -451,11 +506,11 @@ __global__ __launch_bounds__(TL::THREADS) void row_gemm_bf16_kernel(RowGemm g) {
   const int tn = tnc - z * tiles_n1;
   if constexpr (kSplit) {
     if (half >= 0) {
-      row_gemm_tile<TMid, EPI, BUF>(g, tm, tn * 2 + half, z, L0, L1, L2, L3);
+      row_gemm_tile<TMid, EPI, BUF, NOUT == 3>(g, tm, tn * 2 + half, z, L0, L1, L2, L3);
       return;
     }
   }
-  row_gemm_tile<TL, EPI, BUF>(g, tm, tn, z, L0, L1, L2, L3);
+  row_gemm_tile<TL, EPI, BUF, NOUT == 3>(g, tm, tn, z, L0, L1, L2, L3);
 }
 
 // Rounds of a launch of `tiles` tiles on the CUs, in units of a full round
@@ -525,6 +580,8 @@ hipError_t launch_best(const RowGemm& g, hipStream_t s) {
 hipError_t launch_row_gemm_bf16(const RowGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.Nc <= 0 || (g.n_out != 1 && g.n_out != 3)) return hipSuccess;
   if (g.K % TBig::BK || g.K % T192::BK || g.K % TMid::BK) return hipErrorInvalidValue;
+  if (g.rope_cs && g.rope_outs && g.n_out != 3) return hipErrorInvalidValue;  // RoPE: Q/K/V only
+  if (g.residual && g.out[0].c_limit <= 0) return hipSuccess;  // no output row
   if (g.n_out == 3) return launch_best<3, kEpiBf16>(g, s);
   if (g.c_f32) return launch<TMid, 1, kEpiF32>(g, s);
   if (g.gelu) return launch_best<1, kEpiBf16Gelu>(g, s);
