@@ -44,6 +44,9 @@ AS_CASES = [
     (3001, 12, (12, 6, 4, 3, 2, 1), range(12), 0),
     (300001, 40, (40, 20, 10, 5), (0, 1, 2, 3), 0),  # 16 ranges of several 16384-token chunks each
     (4097, 40, (40, 20, 10, 5), (1, 2), 0),          # two ranges, the second of one token
+    (10, 1, (1,), (0,), 0),                           # T = 1: one iteration, every token active
+    (2000, 1024, (1024, 512, 1), (0, 1, 2, 512, 1023), 0),       # the largest T of the LDS table
+    (2000, 1025, (1025, 205, 41, 5, 1), (0, 5, 41, 205, 1024), 0),  # the smallest T past it
 ]
 
 
